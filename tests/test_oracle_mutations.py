@@ -1,0 +1,57 @@
+"""The pins are strong enough to catch plausible mistakes: each case below plants
+one error in a temporary copy of the oracle source, builds it, and requires at
+least one pin to fail against that build (CPU only; the real oracle is untouched)."""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import pins
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle", "ress_oracle.c")
+
+MUTATIONS = {
+    "restore_gain_sign": ("dG = -2.0 * dkMg + s[k] * s[k];", "dG = 2.0 * dkMg + s[k] * s[k];"),
+    "drop_gain_no_s2": ("dG = 2.0 * dkMg + s[k] * s[k];", "dG = 2.0 * dkMg;"),
+    "key_no_renorm": ("key[j] = s[j] / (den > eps ? den : eps);", "key[j] = s[j];"),
+    "tie_to_higher_index": ("return (a->j < b->j) ? -1 : (a->j > b->j);",
+                            "return (a->j > b->j) ? -1 : (a->j < b->j);"),
+    "schedule_off_by_one": ("ldexp(1.0, -(r + 1))", "ldexp(1.0, -r)"),
+    "no_track_best": ("if (J < Jb) {", "if (1) {"),
+    "drift_without_prob": ("g[d] += P[j] * (vbar_i[d] - vbar[(size_t)j * D + d]);",
+                           "g[d] += (vbar_i[d] - vbar[(size_t)j * D + d]);"),
+    "pooled_logit_unscaled": ("    double scale = 1.0 / sqrt((double)D);\n    for (int j = 0; j < nkb; ++j) {",
+                              "    double scale = 1.0;\n    for (int j = 0; j < nkb; ++j) {"),
+    "pool_divides_by_block": ("sum / (double)(hi - lo)", "sum / (double)b"),
+    "attn_unscaled": ("lg[ns] = dot * scale;", "lg[ns] = dot;"),
+    "mass_sign": ("double K = 1.0 - mass;", "double K = 1.0 + mass;"),
+    "drop_gain_uses_plus_u": ("dG = 2.0 * dkMg + s[k] * s[k];\n            u = -P[k];",
+                              "dG = 2.0 * dkMg + s[k] * s[k];\n            u = P[k];"),
+}
+
+
+def _build_mutant(tmp_path, name):
+    old, new = MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique"
+    path = tmp_path / f"{name}.c"
+    path.write_text(src.replace(old, new))
+    lib = tmp_path / f"lib_{name}.so"
+    subprocess.run(["gcc", "-std=c99", "-O1", "-fopenmp", "-fPIC", "-shared", str(path), "-o", str(lib),
+                    "-lm"], check=True)
+    return str(lib)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_pins_catch(name, tmp_path):
+    lib = _build_mutant(tmp_path, name)
+    caught = []
+    with oracle.use_library(lib):
+        for check in pins.ALL:
+            try:
+                check()
+            except AssertionError:
+                caught.append(check.__name__)
+    assert caught, f"no pin caught the planted error {name}"
+    print(name, "caught by", caught)
