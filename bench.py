@@ -1,0 +1,271 @@
+"""Benchmark of one global-attention layer of the ReSS hot path on one MI355X.
+
+One step = ress_select (pooling, drift scores, top-c, R restoration rounds,
+kept lists) + ress_sparse_attn (block-sparse attention over the kept blocks) on
+one synthetic layer whose inputs are already resident in HBM. The default
+workload is 32 views x 1374 tokens (43,968 tokens), 16 heads x 64, blocks of 128,
+75% block sparsity, 5 rounds.
+
+Prints one JSON line (rank 0). Also reports: the dense attention baseline of the
+same library, per-kernel times from HIP events recorded on the launch stream,
+the roofline object of the dominant kernel (block-sparse attention, bf16 MFMA),
+and the CPU oracle timed on a bounded sample of the same layer.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "ms/layer (selection + block-sparse attn) and % bf16 MFMA peak at 32 views"
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparse_attn_32v_traffic.txt")
+ATTN_SRC = os.path.join(ROOT, "paper_2609_35593_amd", "csrc", "attn.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="32v", help="workload: tiny, 8v, 32v, 100v, 16v_stack")
+    ap.add_argument("--sparsity", type=float, default=0.75)
+    ap.add_argument("--rounds", type=int, default=5)
+    ap.add_argument("--dense-steps", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of known size (for HBM counter scaling)")
+    return ap.parse_args()
+
+
+def kept_flops(L, kc, ki):
+    """4 D flops per (query token, kept key token) pair, summed over the layer."""
+    q_len = np.minimum(L.bq, L.N - np.arange(L.n_qb) * L.bq)
+    k_len = np.minimum(L.bk, L.N - np.arange(L.n_kb) * L.bk)
+    kc = kc.reshape(L.H, L.n_qb)
+    ki = ki.reshape(L.H, L.n_qb, L.n_kb)
+    keys = np.where(ki >= 0, k_len[np.clip(ki, 0, None)], 0).sum(axis=2)  # [H][n_qb]
+    return 4.0 * L.D * float((keys * q_len[None, :]).sum()), int(kc.sum())
+
+
+def select_bytes(L):
+    """Algorithmic HBM bytes of one ress_select: Q, K, V read once (bf16); the
+    float64 pooled tensors (qbar, and kbar^T, vbar, vbar^T, M vbar) written once
+    and read once; kept lists (padded to n_kb), counts and drift written once."""
+    qkv = 3.0 * L.H * L.N * L.D * 2
+    pooled = 2.0 * L.H * (L.n_qb + 4 * L.n_kb) * L.D * 8
+    lists = 4.0 * L.H * L.n_qb * (L.n_kb + 1) + 16.0 * L.H * L.n_qb
+    return qkv + pooled + lists
+
+
+def traffic_from_profile():
+    """HBM bytes per sparse-attention launch measured with rocprofv3 counters, if
+    they were taken on the current kernel source (else None)."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()[:16]
+    if vals.get("attn_source_sha256_16") != sha or "hbm_bytes_per_launch" not in vals:
+        return None
+    return float(vals["hbm_bytes_per_launch"])
+
+
+def cpu_baseline(L, rounds, kc_gpu, ki_gpu, budget_s):
+    """The oracle on the host cores: selection of a sample of rows and sparse
+    attention of a sample of query tokens, each scaled to the whole layer."""
+    import oracle
+
+    threads = oracle.max_threads()
+    rng = np.random.default_rng(0)
+    R = L.H * L.n_qb
+    n_rows = min(R, 512)
+    rows = np.sort(rng.choice(R, size=n_rows, replace=False)).astype(np.int32)
+    t0 = time.perf_counter()
+    oracle.select(L.q, L.k, L.v, L.gram, L.budgets, N=L.N, bq=L.bq, bk=L.bk, n_special=L.n_special_tail,
+                  rounds=rounds, rows=rows, want_key=False)
+    t_sel = time.perf_counter() - t0
+    n_tok = 256
+    toks = 0
+    t_attn = 0.0
+    while t_attn < budget_s and toks < L.H * L.N:
+        hs = rng.integers(0, L.H, n_tok).astype(np.int32)
+        ts = rng.integers(0, L.N, n_tok).astype(np.int32)
+        t0 = time.perf_counter()
+        oracle.attn_tokens(L.q, L.k, L.v, N=L.N, bq=L.bq, bk=L.bk, scale=1 / math.sqrt(L.D), sel_h=hs, sel_t=ts,
+                           kept_count=kc_gpu, kept_idx=ki_gpu)
+        t_attn += time.perf_counter() - t0
+        toks += n_tok
+        n_tok *= 2
+    ms = 1e3 * (t_sel * R / n_rows + t_attn * (L.H * L.N) / toks)
+    return {"value": round(ms, 3), "unit": "ms/layer", "cores": threads, "kind": "oracle",
+            "sample": f"selection of {n_rows} of {R} (head, query block) rows and sparse attention of "
+                      f"{toks} of {L.H * L.N} (head, query token) rows, each timed and scaled linearly "
+                      f"to the whole layer (float64, {threads} OpenMP threads)",
+            "measured_seconds": round(t_sel + t_attn, 2)}
+
+
+def copy_calibration():
+    import torch
+
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 5}))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested). Run with --gpus 1.", file=sys.stderr)
+        return 2
+    import torch
+
+    import paper_2609_35593_amd as ress
+    import synth
+
+    if args.copy_calibration:
+        copy_calibration()
+        return 0
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.time()
+    L = synth.make_config(args.config, sparsity=args.sparsity)
+    q, k, v = (ress.bf16_from_bits(x, dev) for x in (L.q, L.k, L.v))
+    gram = torch.from_numpy(L.gram).to(dev)
+    gen_s = time.time() - t_gen
+    n_qb, n_kb = L.n_qb, L.n_kb
+    kc = torch.empty((L.H, n_qb), dtype=torch.int32, device=dev)
+    ki = torch.empty((L.H, n_qb, n_kb), dtype=torch.int32, device=dev)
+    drift = torch.empty((L.H, n_qb, 2), dtype=torch.float64, device=dev)
+    o = torch.empty_like(q)
+    ws = torch.empty(ress.ress_select_workspace_size(
+        ress.make_shape(L.H, L.N, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail)), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        ress.ress_select(q, k, v, gram, L.budgets, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                         rounds=args.rounds, kept_count=kc, kept_idx=ki, drift=drift, workspace=ws, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        ress.ress_sparse_attn(q, k, v, kc, ki, bq=L.bq, bk=L.bk, out=o, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # Timed region: exactly `steps` steps, synchronised on both sides.
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall_ms = 1e3 * (time.perf_counter() - t0) / args.steps
+
+    # Per-kernel durations with events on the launch stream (separate pass).
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    t_sel = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    t_sp = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+
+    # Dense baseline of the same library.
+    od = torch.empty_like(q)
+    ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, out=od, stream=stream)
+    dev_evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.dense_steps)]
+    for a, b in dev_evs:
+        a.record(stream)
+        ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, out=od, stream=stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    t_dense = float(np.mean([a.elapsed_time(b) for a, b in dev_evs]))
+
+    kc_h, ki_h, dr = kc.cpu().numpy(), ki.cpu().numpy(), drift.cpu().numpy().reshape(-1, 2)
+    flops_kept, kept_tiles = kept_flops(L, kc_h, ki_h)
+    flops_dense = 4.0 * L.D * L.H * float(L.N) * float(L.N)
+    tf_kept = flops_kept / (t_sp * 1e-3) / 1e12
+    tf_dense_eq = flops_dense / (wall_ms * 1e-3) / 1e12
+    sel_bytes = select_bytes(L)
+    measured_sparsity = 1.0 - kept_tiles / float(L.H * n_qb * n_kb)
+    ok = dr[:, 0] > 0
+    traffic = traffic_from_profile()
+
+    out = {
+        "metric": METRIC,
+        "value": round(wall_ms, 4),
+        "unit": "ms/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.config}: one global-attention layer, {L.N} tokens "
+                        f"({L.H} heads x {L.D}), blocks {L.bq}/{L.bk}, {n_qb}x{n_kb} blocks per head, "
+                        f"target sparsity {args.sparsity}, {args.rounds} restoration rounds",
+            "tokens": L.N, "heads": L.H, "head_dim": L.D, "block": L.bq, "sparsity_target": args.sparsity,
+            "rounds": args.rounds, "select_dtype": "f64", "attention_dtype": "bf16 MFMA, f32 accumulate",
+        },
+        "roofline": {
+            "kernel": "attn_kernel<128,128,sparse> (ress_sparse_attn)",
+            "bound": "mfma",
+            "achieved": round(tf_kept, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(tf_kept / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "algorithmic_flops_per_launch": flops_kept,
+        },
+        "breakdown": {
+            "select_ms": round(t_sel, 4),
+            "sparse_attn_ms": round(t_sp, 4),
+            "selection_overhead_frac": round(t_sel / (t_sel + t_sp), 4),
+            "dense_attn_ms": round(t_dense, 4),
+            "speedup_vs_dense": round(t_dense / wall_ms, 3),
+            "dense_tflops": round(flops_dense / (t_dense * 1e-3) / 1e12, 2),
+            "dense_frac_peak": round(flops_dense / (t_dense * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "dense_equivalent_tflops": round(tf_dense_eq, 2),
+            "kept_only_tflops": round(tf_kept, 2),
+            "select_gbs": round(sel_bytes / (t_sel * 1e-3) / 1e9, 1),
+            "select_frac_hbm": round(sel_bytes / (t_sel * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "measured_sparsity": round(measured_sparsity, 4),
+            "J_best_over_J_init_median": round(float(np.median(dr[ok, 1] / dr[ok, 0])), 4) if ok.any() else None,
+            "input_generation_s": round(gen_s, 1),
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(L, args.rounds, kc_h, ki_h, args.cpu_seconds)
+        out["cpu_baseline"]["gpu_speedup"] = round(out["cpu_baseline"]["value"] / wall_ms, 1)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,139 @@
+/*
+ * ress.h - C ABI of the MI355X (gfx950) hot path of ReSS, "Residual-Restoring
+ * Sparse Attention for 3D Vision Transformers": drift-based block selection
+ * followed by block-sparse attention over the kept blocks, plus the dense
+ * attention it is measured against.
+ *
+ * Conventions shared by every entry point
+ *  - Tensors Q, K, V, O are bf16, laid out [H][N][D] contiguous (head-major, then
+ *    token, then channel), one layer of batch 1, with D == 64.
+ *  - Tokens are grouped into fixed-size blocks: query block i covers tokens
+ *    [i*bq, min((i+1)*bq, N)), key block j covers [j*bk, min((j+1)*bk, N))
+ *    (the paper's block grid, Sec. 3 step (1)); the last block of each kind may be
+ *    partial. n_qb = ceil(N / bq), n_kb = ceil(N / bk).
+ *  - The last n_special_tail tokens are special (camera / register) tokens. Key
+ *    blocks that hold any of them are always kept and are not candidates
+ *    (Sec. 4.1; the trailing "sink" block of Supp. F).
+ *  - Device pointers are owned by the caller; the library never allocates,
+ *    frees or copies device memory and never synchronises. All work is enqueued
+ *    on `stream` in order; a status of RESS_OK means the work was enqueued.
+ *    Device-side failures surface at the caller's next synchronisation.
+ *  - On any error status nothing is enqueued and no output is written.
+ *  - Calls are stateless; concurrent calls on different streams are safe as
+ *    long as their output buffers (and workspaces) do not overlap.
+ */
+#ifndef RESS_H
+#define RESS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define RESS_OK 0
+#define RESS_E_INVALID_ARG (-1) /* null pointer, negative size, bad parameter or budget */
+#define RESS_E_UNSUPPORTED (-2) /* D != 64, block size not 64/128, n_kb > 4096, H > 256 */
+#define RESS_E_WORKSPACE (-3)   /* workspace missing, too small or misaligned */
+#define RESS_E_HIP (-4)         /* a HIP launch call failed */
+
+/* Largest number of key blocks per row: one row of the selection is held in
+ * registers, the same cap as the paper's fused round kernel (Supp. E). */
+#define RESS_MAX_KEY_BLOCKS 4096
+#define RESS_MAX_HEADS 256
+#define RESS_MAX_ROUNDS 32
+
+typedef struct {
+    int H;              /* heads, 0..RESS_MAX_HEADS */
+    int N;              /* tokens per head (all views concatenated), >= 0 */
+    int D;              /* head dimension; must be 64 */
+    int bq;             /* query block size: 64 or 128 */
+    int bk;             /* key block size: 64 or 128 */
+    int n_special_tail; /* trailing special tokens, 0..N */
+} ress_shape;
+
+/* Selection parameters (Secs. 4.2-4.3). The paper's values: rounds = 5,
+ * rho = 0.5, eps = 1e-4 (Eqs. 7 and 17). */
+typedef struct {
+    int rounds;                /* restoration rounds R, 0..RESS_MAX_ROUNDS */
+    double rho;                /* total swap budget as a fraction of c_h (Eq. 17), >= 0 */
+    double eps;                /* guard of Eq. 7, also applied to K in J and dJ, > 0 */
+    int swap_floor;            /* round r swaps max(swap_floor, floor(rho c_h 2^-(r+1))), >= 0 */
+    int dense_special_queries; /* nonzero: query blocks holding special tokens keep every key block */
+} ress_select_params;
+
+/* Bytes of device workspace ress_select needs for `shape` (pooled tensors,
+ * float64). Returns RESS_OK, or RESS_E_INVALID_ARG / RESS_E_UNSUPPORTED. */
+int ress_select_workspace_size(const ress_shape *shape, size_t *bytes);
+
+/* Drift-based block selection (Secs. 4.2-4.3): for every head h and query
+ * block i,
+ *   1. pool Q, K, V into block means (Sec. 3 step (1));
+ *   2. P_i = softmax_j(Qbar_i . Kbar_j / sqrt(D)) over all key blocks and the
+ *      dense pooled output vbar_i = sum_j P_ij Vbar_j (Eq. 1);
+ *   3. score every candidate key block by s_ij = P_ij ||W_O^h (vbar_i - Vbar_j)||
+ *      through the Gram matrix M_h = W_O^h^T W_O^h (Eqs. 5-9) and keep the c_h
+ *      largest keys s_ij / max(1 - P_ij, eps) (Eq. 7);
+ *   4. run `rounds` budget-neutral rounds that restore the m_r dropped blocks and
+ *      drop the m_r kept candidates with the largest exact decrease of the drift
+ *      objective J = g^T M g / K^2 (Eqs. 10-17), keeping the drop set with the
+ *      smallest J seen, the initial one included (track-best).
+ * Every top-k breaks ties by the lower block index. Scoring and restoration run
+ * in float64.
+ *
+ *   q, k, v       device bf16 [H][N][D]
+ *   gram          device float32 [H][D][D], M_h row-major (computed once at load,
+ *                 Eq. 8); used as given, M_h x means sum_b M[a][b] x[b]
+ *   keep_budget   HOST int32 [H]: c_h, kept candidate blocks per row. Must lie in
+ *                 [min(n_p, max(0, 2 - n_forced)), n_p], n_p = candidates (the
+ *                 paper's floor of two kept key blocks per query row, Supp. F)
+ *   kept_count    device int32 [H][n_qb] out: kept key blocks per row
+ *                 (c_h + n_forced, or n_kb for dense rows)
+ *   kept_idx      device int32 [H][n_qb][n_kb] out: kept key block indices in
+ *                 ascending order, padded with -1
+ *   drift         device float64 [H][n_qb][2] out (or NULL): (J of the initial
+ *                 selection, J of the returned selection); 0 for rows that drop
+ *                 nothing
+ *   key_out       device float64 [H][n_qb][n_kb] out (or NULL): ranking keys of
+ *                 Eq. 7; -1 for forced blocks
+ *   prob_out      device float64 [H][n_qb][n_kb] out (or NULL): pooled map P
+ *   workspace     device, >= ress_select_workspace_size bytes, 256-byte aligned
+ * Inputs must be finite; non-finite inputs give unspecified (but in-bounds)
+ * selections. */
+int ress_select(const ress_shape *shape, const ress_select_params *params, const void *q,
+                const void *k, const void *v, const float *gram, const int32_t *keep_budget,
+                int32_t *kept_count, int32_t *kept_idx, double *drift, double *key_out,
+                double *prob_out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Block-sparse attention (Sec. 3 step (3)): every query token t of query block
+ * i attends exactly to the tokens of the key blocks kept_idx[h][i][0 ..
+ * kept_count[h][i]-1], with the softmax renormalised among them:
+ *   O_t = sum_s softmax_s(scale * Q_t . K_s) V_s.
+ * bf16 MFMA products, float32 softmax and accumulation.
+ *   kept_count  device int32 [H][n_qb]; values are clamped to [0, n_kb]
+ *   kept_idx    device int32 [H][n_qb][n_kb]; entries outside [0, n_kb) are
+ *               ignored (contribute no keys); duplicates count twice
+ *   scale       softmax scale, normally 1/sqrt(D); must be finite
+ *   o           device bf16 [H][N][D] out (must not alias q, k, v)
+ * A row with no keys gets a zero output. */
+int ress_sparse_attn(const ress_shape *shape, const void *q, const void *k, const void *v,
+                     const int32_t *kept_count, const int32_t *kept_idx, float scale, void *o,
+                     hipStream_t stream);
+
+/* Dense attention, the same computation over every key block of every row
+ * (the baseline the paper compares against, Table S6). */
+int ress_dense_attn(const ress_shape *shape, const void *q, const void *k, const void *v,
+                    float scale, void *o, hipStream_t stream);
+
+/* Human-readable name of a status code (static string). */
+const char *ress_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RESS_H */

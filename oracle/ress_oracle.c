@@ -361,7 +361,9 @@ void ro_select_row(int D, int nkb, const double *qbar_i, const double *kbar,
         free(restore);
         free(drop);
         J = ro_objective(D, nkb, P, vbar_i, vbar, M, inD, eps, NULL, NULL, NULL);
-        mrg = min2(mrg, fabs(J - Jb) / (Jb > 0.0 ? Jb : 1e-300));
+        /* The track-best comparison decides the output only when this stage's
+         * drop set differs from the best one (a set revisited has the same J). */
+        if (memcmp(inD, best, nkb) != 0) mrg = min2(mrg, fabs(J - Jb) / (Jb > 0.0 ? Jb : 1e-300));
         if (J < Jb) {
             Jb = J;
             memcpy(best, inD, nkb);

@@ -1,0 +1,188 @@
+"""Python binding of libress, the MI355X (gfx950) hot path of ReSS.
+
+Thin ctypes marshalling over the C ABI in include/ress.h; the functions carry
+the C entry points' names. Every step of the path runs in the HIP kernels of
+libress.so: this module only checks tensor metadata, allocates outputs with
+torch when the caller passes none, and passes pointers and the current stream.
+There is no fallback: if libress.so is missing the import fails.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libress.so")
+
+RESS_OK = 0
+RESS_E_INVALID_ARG = -1
+RESS_E_UNSUPPORTED = -2
+RESS_E_WORKSPACE = -3
+RESS_E_HIP = -4
+MAX_KEY_BLOCKS = 4096
+
+
+class ress_shape(C.Structure):
+    _fields_ = [("H", C.c_int), ("N", C.c_int), ("D", C.c_int), ("bq", C.c_int), ("bk", C.c_int),
+                ("n_special_tail", C.c_int)]
+
+
+class ress_select_params(C.Structure):
+    _fields_ = [("rounds", C.c_int), ("rho", C.c_double), ("eps", C.c_double), ("swap_floor", C.c_int),
+                ("dense_special_queries", C.c_int)]
+
+
+class RessError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -c 'import __graft_entry__ as g; g.build()'` "
+                          "or `python paper_2609_35593_amd/build.py`")
+    L = C.CDLL(LIB_PATH)
+    vp, i, f, sz = C.c_void_p, C.c_int, C.c_float, C.c_size_t
+    L.ress_status_string.argtypes = [i]
+    L.ress_status_string.restype = C.c_char_p
+    L.ress_select_workspace_size.argtypes = [C.POINTER(ress_shape), C.POINTER(sz)]
+    L.ress_select_workspace_size.restype = i
+    L.ress_select.argtypes = [C.POINTER(ress_shape), C.POINTER(ress_select_params), vp, vp, vp, vp, vp, vp, vp,
+                              vp, vp, vp, vp, sz, vp]
+    L.ress_select.restype = i
+    L.ress_sparse_attn.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, f, vp, vp]
+    L.ress_sparse_attn.restype = i
+    L.ress_dense_attn.argtypes = [C.POINTER(ress_shape), vp, vp, vp, f, vp, vp]
+    L.ress_dense_attn.restype = i
+    return L
+
+
+lib = _load()
+
+
+def status_string(status: int) -> str:
+    return lib.ress_status_string(int(status)).decode()
+
+
+ress_status_string = status_string
+
+
+def make_shape(H: int, N: int, *, bq: int, bk: int, n_special_tail: int = 0, D: int = 64) -> ress_shape:
+    return ress_shape(int(H), int(N), int(D), int(bq), int(bk), int(n_special_tail))
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _stream(stream, device) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _check_qkv(q, k, v):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not (t.is_cuda and t.dtype == torch.bfloat16 and t.is_contiguous() and t.dim() == 3):
+            raise ValueError(f"{name} must be a contiguous CUDA bfloat16 tensor [H][N][D]")
+    if not (q.shape == k.shape == v.shape) or q.device != k.device or q.device != v.device:
+        raise ValueError("q, k, v must share shape and device")
+
+
+def ress_select_workspace_size(shape: ress_shape) -> int:
+    n = C.c_size_t(0)
+    st = lib.ress_select_workspace_size(C.byref(shape), C.byref(n))
+    if st != RESS_OK:
+        raise RessError(st, "ress_select_workspace_size")
+    return n.value
+
+
+def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail: int = 0,
+                rounds: int = 5, rho: float = 0.5, eps: float = 1e-4, swap_floor: int = 1,
+                dense_special_queries: bool = True, kept_count=None, kept_idx=None, drift=None,
+                key_out=None, prob_out=None, want_drift: bool = True, want_debug: bool = False,
+                workspace=None, stream=None) -> dict:
+    """Drift-based block selection for one layer (see include/ress.h).
+    keep_budget: host int32 [H]. Returns the output tensors in a dict."""
+    _check_qkv(q, k, v)
+    H, N, D = q.shape
+    shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
+    n_qb, n_kb = (N + bq - 1) // bq, (N + bk - 1) // bk
+    dev = q.device
+    if not (gram.is_cuda and gram.dtype == torch.float32 and gram.is_contiguous() and gram.shape == (H, D, D)):
+        raise ValueError("gram must be a contiguous CUDA float32 tensor [H][D][D]")
+    budget = np.ascontiguousarray(np.asarray(keep_budget, dtype=np.int32).reshape(-1))
+    if budget.shape[0] != H:
+        raise ValueError("keep_budget must hold one int per head")
+    if kept_count is None:
+        kept_count = torch.empty((H, n_qb), dtype=torch.int32, device=dev)
+    if kept_idx is None:
+        kept_idx = torch.empty((H, n_qb, n_kb), dtype=torch.int32, device=dev)
+    if drift is None and want_drift:
+        drift = torch.empty((H, n_qb, 2), dtype=torch.float64, device=dev)
+    if want_debug:
+        if key_out is None:
+            key_out = torch.empty((H, n_qb, n_kb), dtype=torch.float64, device=dev)
+        if prob_out is None:
+            prob_out = torch.empty((H, n_qb, n_kb), dtype=torch.float64, device=dev)
+    need = ress_select_workspace_size(shape)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    params = ress_select_params(int(rounds), float(rho), float(eps), int(swap_floor), int(bool(dense_special_queries)))
+    st = lib.ress_select(C.byref(shape), C.byref(params), _ptr(q), _ptr(k), _ptr(v), _ptr(gram),
+                         budget.ctypes.data, _ptr(kept_count), _ptr(kept_idx), _ptr(drift), _ptr(key_out),
+                         _ptr(prob_out), _ptr(workspace), workspace.numel(), _stream(stream, dev))
+    if st != RESS_OK:
+        raise RessError(st, "ress_select")
+    return dict(kept_count=kept_count, kept_idx=kept_idx, drift=drift, key=key_out, prob=prob_out)
+
+
+def ress_sparse_attn(q, k, v, kept_count, kept_idx, *, bq: int, bk: int, n_special_tail: int = 0,
+                     scale: float | None = None, out=None, stream=None):
+    """Block-sparse attention over the kept key blocks (see include/ress.h)."""
+    _check_qkv(q, k, v)
+    H, N, D = q.shape
+    shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
+    for t in (kept_count, kept_idx):
+        if not (t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()):
+            raise ValueError("kept_count / kept_idx must be contiguous CUDA int32 tensors")
+    n_qb, n_kb = (N + bq - 1) // bq, (N + bk - 1) // bk
+    if kept_count.numel() != H * n_qb or kept_idx.numel() != H * n_qb * n_kb:
+        raise ValueError("kept_count must be [H][n_qb] and kept_idx [H][n_qb][n_kb]")
+    if out is None:
+        out = torch.empty_like(q)
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    st = lib.ress_sparse_attn(C.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(kept_count), _ptr(kept_idx),
+                              float(scale), _ptr(out), _stream(stream, q.device))
+    if st != RESS_OK:
+        raise RessError(st, "ress_sparse_attn")
+    return out
+
+
+def ress_dense_attn(q, k, v, *, bq: int, bk: int, n_special_tail: int = 0, scale: float | None = None,
+                    out=None, stream=None):
+    """Dense attention over every key block (see include/ress.h)."""
+    _check_qkv(q, k, v)
+    H, N, D = q.shape
+    shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
+    if out is None:
+        out = torch.empty_like(q)
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    st = lib.ress_dense_attn(C.byref(shape), _ptr(q), _ptr(k), _ptr(v), float(scale), _ptr(out),
+                             _stream(stream, q.device))
+    if st != RESS_OK:
+        raise RessError(st, "ress_dense_attn")
+    return out
+
+
+def bf16_from_bits(bits: np.ndarray, device) -> torch.Tensor:
+    """Device bf16 tensor holding the given uint16 bit patterns."""
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.view(torch.bfloat16).to(device)

@@ -1,0 +1,198 @@
+// C ABI of libress: argument validation, workspace layout and kernel launches.
+// Every check runs on the host before anything is enqueued, so an error status
+// means no device work and no output writes.
+#include <math.h>
+#include <string.h>
+
+#include "ress_internal.h"
+
+namespace {
+
+using ress::kD;
+
+struct Grid {
+    long long n_qb, n_kb;
+};
+
+int check_shape(const ress_shape *s, Grid *g)
+{
+    if (!s) return RESS_E_INVALID_ARG;
+    if (s->H < 0 || s->N < 0 || s->n_special_tail < 0 || s->n_special_tail > s->N) return RESS_E_INVALID_ARG;
+    if (s->D != kD) return RESS_E_UNSUPPORTED;
+    if ((s->bq != 64 && s->bq != 128) || (s->bk != 64 && s->bk != 128)) return RESS_E_UNSUPPORTED;
+    if (s->H > RESS_MAX_HEADS) return RESS_E_UNSUPPORTED;
+    g->n_qb = ((long long)s->N + s->bq - 1) / s->bq;
+    g->n_kb = ((long long)s->N + s->bk - 1) / s->bk;
+    return RESS_OK;
+}
+
+bool has_work(const ress_shape *s) { return s->H > 0 && s->N > 0; }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace: qbar [H][n_qb][64], then kbarT, vbar, vbarT, uT, each [H][n_kb][64]
+// (float64), every region 256-byte aligned.
+size_t workspace_bytes(const ress_shape *s, const Grid &g)
+{
+    const size_t qb = align256((size_t)s->H * g.n_qb * kD * sizeof(double));
+    const size_t kb = align256((size_t)s->H * g.n_kb * kD * sizeof(double));
+    return qb + 4 * kb;
+}
+
+int first_forced_block(const ress_shape *s, const Grid &g)
+{
+    return s->n_special_tail > 0 ? (s->N - s->n_special_tail) / s->bk : (int)g.n_kb;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ress_status_string(int status)
+{
+    switch (status) {
+    case RESS_OK: return "RESS_OK";
+    case RESS_E_INVALID_ARG: return "RESS_E_INVALID_ARG: invalid argument";
+    case RESS_E_UNSUPPORTED: return "RESS_E_UNSUPPORTED: unsupported shape (D must be 64, blocks 64/128, n_kb <= 4096, H <= 256)";
+    case RESS_E_WORKSPACE: return "RESS_E_WORKSPACE: workspace missing, too small or not 256-byte aligned";
+    case RESS_E_HIP: return "RESS_E_HIP: HIP launch failed";
+    default: return "unknown ress status";
+    }
+}
+
+int ress_select_workspace_size(const ress_shape *shape, size_t *bytes)
+{
+    Grid g;
+    int st = check_shape(shape, &g);
+    if (st != RESS_OK) return st;
+    if (!bytes) return RESS_E_INVALID_ARG;
+    if (g.n_kb > RESS_MAX_KEY_BLOCKS) return RESS_E_UNSUPPORTED;
+    *bytes = has_work(shape) ? workspace_bytes(shape, g) : 0;
+    return RESS_OK;
+}
+
+int ress_select(const ress_shape *shape, const ress_select_params *params, const void *q,
+                const void *k, const void *v, const float *gram, const int32_t *keep_budget,
+                int32_t *kept_count, int32_t *kept_idx, double *drift, double *key_out,
+                double *prob_out, void *workspace, size_t ws_bytes, hipStream_t stream)
+{
+    Grid g;
+    int st = check_shape(shape, &g);
+    if (st != RESS_OK) return st;
+    if (g.n_kb > RESS_MAX_KEY_BLOCKS) return RESS_E_UNSUPPORTED;
+    if (!params) return RESS_E_INVALID_ARG;
+    if (params->rounds < 0 || params->rounds > RESS_MAX_ROUNDS || params->swap_floor < 0 ||
+        !(params->rho >= 0.0) || !isfinite(params->rho) || !(params->eps > 0.0) || !isfinite(params->eps))
+        return RESS_E_INVALID_ARG;
+    if (!has_work(shape)) return RESS_OK;
+    if (!q || !k || !v || !gram || !keep_budget || !kept_count || !kept_idx) return RESS_E_INVALID_ARG;
+
+    const int n_kb = (int)g.n_kb, n_qb = (int)g.n_qb;
+    const int first_forced = first_forced_block(shape, g);
+    const int n_forced = n_kb - first_forced, n_p = first_forced;
+    const int floor2 = 2 - n_forced > 0 ? 2 - n_forced : 0;  // at least two kept blocks per row
+    const int lo = n_p < floor2 ? n_p : floor2;
+    for (int h = 0; h < shape->H; ++h)
+        if (keep_budget[h] < lo || keep_budget[h] > n_p) return RESS_E_INVALID_ARG;
+
+    const size_t need = workspace_bytes(shape, g);
+    if (!workspace || ws_bytes < need || ((uintptr_t)workspace & 255u)) return RESS_E_WORKSPACE;
+
+    ress::Pooled pooled;
+    {
+        char *w = static_cast<char *>(workspace);
+        const size_t qb = align256((size_t)shape->H * n_qb * kD * sizeof(double));
+        const size_t kb = align256((size_t)shape->H * n_kb * kD * sizeof(double));
+        pooled.qbar = reinterpret_cast<double *>(w);
+        pooled.kbarT = reinterpret_cast<double *>(w + qb);
+        pooled.vbar = reinterpret_cast<double *>(w + qb + kb);
+        pooled.vbarT = reinterpret_cast<double *>(w + qb + 2 * kb);
+        pooled.uT = reinterpret_cast<double *>(w + qb + 3 * kb);
+    }
+
+    ress::PoolParams pp;
+    pp.H = shape->H;
+    pp.N = shape->N;
+    pp.bq = shape->bq;
+    pp.bk = shape->bk;
+    pp.n_qb = n_qb;
+    pp.n_kb = n_kb;
+    pp.q = static_cast<const uint16_t *>(q);
+    pp.k = static_cast<const uint16_t *>(k);
+    pp.v = static_cast<const uint16_t *>(v);
+    pp.gram = gram;
+    pp.out = pooled;
+
+    ress::SelectParams sp;
+    memset(&sp, 0, sizeof sp);
+    sp.H = shape->H;
+    sp.n_qb = n_qb;
+    sp.n_kb = n_kb;
+    sp.first_forced = first_forced;
+    sp.first_dense_qb = (params->dense_special_queries && shape->n_special_tail > 0)
+                            ? (shape->N - shape->n_special_tail) / shape->bq
+                            : n_qb;
+    sp.rounds = params->rounds;
+    sp.swap_floor = params->swap_floor;
+    sp.rho = params->rho;
+    sp.eps = params->eps;
+    sp.pooled = pooled;
+    sp.gram = gram;
+    sp.kept_count = kept_count;
+    sp.kept_idx = kept_idx;
+    sp.drift = drift;
+    sp.key_out = key_out;
+    sp.prob_out = prob_out;
+    for (int h = 0; h < shape->H; ++h) sp.budgets[h] = keep_budget[h];
+
+    if (ress::launch_pool(pp, stream) != hipSuccess) return RESS_E_HIP;
+    if (ress::launch_select(sp, stream) != hipSuccess) return RESS_E_HIP;
+    return RESS_OK;
+}
+
+static int attn_common(const ress_shape *shape, const void *q, const void *k, const void *v,
+                       const int32_t *kept_count, const int32_t *kept_idx, float scale, void *o,
+                       bool sparse, hipStream_t stream)
+{
+    Grid g;
+    int st = check_shape(shape, &g);
+    if (st != RESS_OK) return st;
+    if (!(scale > 0.f) || !isfinite(scale)) return RESS_E_INVALID_ARG;
+    if (!has_work(shape)) return RESS_OK;
+    if (!q || !k || !v || !o) return RESS_E_INVALID_ARG;
+    if (o == q || o == k || o == v) return RESS_E_INVALID_ARG;
+    if (sparse && (!kept_count || !kept_idx)) return RESS_E_INVALID_ARG;
+    const long long items = (long long)shape->H * g.n_qb;
+    const long long per_xcd = (items + 7) / 8;
+    if (8 * per_xcd > 0x7fffffffLL) return RESS_E_UNSUPPORTED;
+    ress::AttnParams ap;
+    ap.H = shape->H;
+    ap.N = shape->N;
+    ap.n_qb = (int)g.n_qb;
+    ap.n_kb = (int)g.n_kb;
+    ap.items_per_xcd = (int)per_xcd;
+    ap.scale_log2 = scale * 1.4426950408889634f;
+    ap.q = static_cast<const uint16_t *>(q);
+    ap.k = static_cast<const uint16_t *>(k);
+    ap.v = static_cast<const uint16_t *>(v);
+    ap.o = static_cast<uint16_t *>(o);
+    ap.kept_count = kept_count;
+    ap.kept_idx = kept_idx;
+    if (ress::launch_attn(ap, shape->bq, shape->bk, sparse, stream) != hipSuccess) return RESS_E_HIP;
+    return RESS_OK;
+}
+
+int ress_sparse_attn(const ress_shape *shape, const void *q, const void *k, const void *v,
+                     const int32_t *kept_count, const int32_t *kept_idx, float scale, void *o,
+                     hipStream_t stream)
+{
+    return attn_common(shape, q, k, v, kept_count, kept_idx, scale, o, true, stream);
+}
+
+int ress_dense_attn(const ress_shape *shape, const void *q, const void *k, const void *v, float scale,
+                    void *o, hipStream_t stream)
+{
+    return attn_common(shape, q, k, v, nullptr, nullptr, scale, o, false, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,57 @@
+// Internal declarations shared by the HIP kernels and the C ABI layer of libress.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/ress.h"
+
+namespace ress {
+
+constexpr int kD = 64;      // head dimension handled by every kernel
+constexpr int kWave = 64;   // CDNA wavefront width
+
+// Pooled tensors of one layer, float64, carved out of the selection workspace.
+struct Pooled {
+    double *qbar;   // [H][n_qb][64]   query block means
+    double *kbarT;  // [H][64][n_kb]   key block means, channel-major
+    double *vbar;   // [H][n_kb][64]   value block means
+    double *vbarT;  // [H][64][n_kb]   value block means, channel-major
+    double *uT;     // [H][64][n_kb]   M_h Vbar_j, channel-major
+};
+
+struct PoolParams {
+    int H, N, bq, bk, n_qb, n_kb;
+    const uint16_t *q, *k, *v;  // bf16 bits [H][N][64]
+    const float *gram;          // [H][64][64]
+    Pooled out;
+};
+
+struct SelectParams {
+    int H, n_qb, n_kb;
+    int first_forced;    // key blocks j >= first_forced are always kept (n_kb if none)
+    int first_dense_qb;  // query blocks i >= first_dense_qb keep every block (n_qb if none)
+    int rounds, swap_floor;
+    double rho, eps;
+    Pooled pooled;
+    const float *gram;
+    int32_t *kept_count, *kept_idx;
+    double *drift, *key_out, *prob_out;
+    int32_t budgets[RESS_MAX_HEADS];
+};
+
+struct AttnParams {
+    int H, N, n_qb, n_kb;
+    int items_per_xcd;  // work items assigned to each of the 8 XCDs
+    float scale_log2;   // softmax scale * log2(e)
+    const uint16_t *q, *k, *v;
+    uint16_t *o;
+    const int32_t *kept_count, *kept_idx;  // null for dense attention
+};
+
+hipError_t launch_pool(const PoolParams &p, hipStream_t s);
+hipError_t launch_select(const SelectParams &p, hipStream_t s);
+hipError_t launch_attn(const AttnParams &p, int bq, int bk, bool sparse, hipStream_t s);
+
+}  // namespace ress

@@ -1,0 +1,273 @@
+"""GPU parity: the HIP path, called through the C ABI, against the float64 oracle
+on the same seeded inputs. Tolerances are documented in gpu_helpers.py."""
+import functools
+import math
+
+import numpy as np
+import pytest
+
+import synth
+from gpu_helpers import (compare_attn, compare_select, device_inputs, gpu_select, oracle_select,
+                         sample_tokens, say)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ress():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_35593_amd as r
+
+    return r
+
+
+@functools.lru_cache(maxsize=None)
+def small(name):
+    if name == "s64":  # no special tokens, 6 blocks of 64
+        return synth.make_layer(4, 96, 0, H=2, block=64, sparsity=0.5, seed=21, name=name)
+    if name == "ragged128x64":  # partial query and key blocks, forced tail blocks
+        return synth.make_layer(3, 150, 5, H=3, bq=128, bk=64, sparsity=0.6, seed=22, name=name)
+    if name == "ragged64x128":
+        return synth.make_layer(5, 201, 5, H=2, bq=64, bk=128, sparsity=0.5, seed=23, name=name)
+    if name == "forced64":  # 20 key blocks of 64, two forced
+        return synth.make_layer(6, 200, 5, H=4, block=64, sparsity=0.6, seed=24, name=name)
+    if name == "b128":  # 1374-token views, block 128
+        return synth.make_layer(3, 1369, 5, H=4, block=128, sparsity=0.75, seed=25, name=name)
+    raise KeyError(name)
+
+
+SMALL = ["s64", "ragged128x64", "ragged64x128", "forced64", "b128"]
+
+
+def _all_tokens(L):
+    hs, ts = np.meshgrid(np.arange(L.H), np.arange(L.N), indexing="ij")
+    return hs.ravel().astype(np.int32), ts.ravel().astype(np.int32)
+
+
+@pytest.mark.parametrize("name", SMALL + ["tiny"])
+def test_dense_attention_small(ress, name):
+    L = small(name) if name != "tiny" else synth.make_config("tiny")
+    say(f"[dense attention] {name} H={L.H} N={L.N} bq={L.bq} bk={L.bk}")
+    q, k, v, _ = device_inputs(L)
+    o = ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk)
+    hs, ts = _all_tokens(L)
+    compare_attn(L, o, hs, ts, label=name)
+
+
+@pytest.mark.parametrize("name", SMALL + ["tiny"])
+def test_select_and_sparse_small(ress, name):
+    import torch
+
+    L = small(name) if name != "tiny" else synth.make_config("tiny")
+    rounds = 3 if name == "tiny" else 5
+    say(f"[select+sparse] {name} H={L.H} N={L.N} n_kb={L.n_kb} budgets={L.budgets.tolist()}")
+    inputs = device_inputs(L)
+    gpu, dev = gpu_select(L, inputs, rounds=rounds)
+    ref = oracle_select(L, rounds=rounds)
+    compare_select(L, gpu, ref, label=name)
+    q, k, v, _ = inputs
+    o = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk)
+    torch.cuda.synchronize()
+    hs, ts = _all_tokens(L)
+    compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label=name + " sparse")
+
+
+@pytest.mark.parametrize("rounds", [0, 1, 2, 7])
+@pytest.mark.parametrize("frac", [0.0, 0.3, 0.9, 1.0])
+def test_select_budgets_and_rounds(ress, rounds, frac):
+    L = small("forced64")
+    nf = synth.forced_block_count(L.N, L.bk, L.n_special_tail)
+    n_p = L.n_kb - nf
+    budgets = np.array([int(round(frac * n_p))] * L.H, np.int32)
+    budgets[0] = min(n_p, budgets[0] + 1)
+    say(f"[select budgets] rounds={rounds} budgets={budgets.tolist()}")
+    gpu, _ = gpu_select(L, rounds=rounds, budgets=budgets)
+    ref = oracle_select(L, rounds=rounds, budgets=budgets)
+    compare_select(L, gpu, ref, budgets=budgets, label=f"R={rounds} frac={frac}")
+
+
+def test_select_without_dense_special_rows(ress):
+    L = small("b128")
+    say("[select] special query rows selected like the others")
+    gpu, _ = gpu_select(L, rounds=5, dense_special_queries=False)
+    ref = oracle_select(L, rounds=5, dense_special_queries=False)
+    compare_select(L, gpu, ref, label="no dense special rows", dense_special_queries=False)
+
+
+def test_zero_sparsity_sparse_equals_dense(ress):
+    import torch
+
+    L = small("b128")
+    nf = synth.forced_block_count(L.N, L.bk, L.n_special_tail)
+    budgets = np.full(L.H, L.n_kb - nf, np.int32)
+    say("[zero sparsity] kept lists are every block; sparse == dense bitwise")
+    q, k, v, gram = device_inputs(L)
+    gpu, dev = gpu_select(L, (q, k, v, gram), budgets=budgets)
+    assert np.all(gpu["kept_count"] == L.n_kb) and np.all(gpu["drift"] == 0)
+    o_s = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk)
+    o_d = ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk)
+    torch.cuda.synchronize()
+    assert torch.equal(o_s, o_d)
+
+
+# ------------------------------------------------------------------ the five workloads
+
+
+def _config_case(ress, L, rounds, rows=None, n_tokens=512, label=""):
+    import torch
+
+    say(f"[{label}] H={L.H} N={L.N} n_qb={L.n_qb} n_kb={L.n_kb} R={rounds} "
+        f"budgets={sorted(set(L.budgets.tolist()))[:6]}")
+    inputs = device_inputs(L)
+    gpu, dev = gpu_select(L, inputs, rounds=rounds)
+    ref = oracle_select(L, rounds=rounds, rows=rows)
+    st = compare_select(L, gpu, ref, rows=rows, label=label)
+    q, k, v, _ = inputs
+    o = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk)
+    torch.cuda.synchronize()
+    hs, ts = sample_tokens(L, n_tokens)
+    compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label=label + " sparse")
+    return st
+
+
+@pytest.mark.parametrize("sparsity", [0.5, 0.75])
+def test_config_8v(ress, sparsity):
+    _config_case(ress, synth.make_config("8v", sparsity=sparsity), 5, label=f"8v s={sparsity}")
+
+
+@pytest.mark.parametrize("sparsity,rounds", [(0.75, 1), (0.75, 3), (0.75, 5), (0.9, 5)])
+def test_config_32v(ress, sparsity, rounds):
+    _config_case(ress, synth.make_config("32v", sparsity=sparsity), rounds, label=f"32v s={sparsity} R={rounds}")
+
+
+def test_config_100v_ragged(ress):
+    L = synth.make_config("100v")
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 400),
+                                     [h * L.n_qb + i for h in range(L.H) for i in (0, L.n_qb - 1, L.n_qb - 6)]]))
+    _config_case(ress, L, 5, rows=rows, n_tokens=256, label="100v ragged")
+
+
+@pytest.mark.parametrize("layer", [0, 7, 15, 23])
+def test_config_layer_stack(ress, layer):
+    _config_case(ress, synth.make_config("16v_stack", layer=layer), 5, n_tokens=256, label=f"16v layer {layer}")
+
+
+def test_dense_attention_32v_sampled(ress):
+    L = synth.make_config("32v")
+    say("[dense attention] 32v sampled tokens")
+    q, k, v, _ = device_inputs(L)
+    o = ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk)
+    hs, ts = sample_tokens(L, 256)
+    compare_attn(L, o, hs, ts, label="32v dense")
+
+
+# ------------------------------------------------------------------ properties, edges
+
+
+def test_reruns_are_bit_identical(ress):
+    import torch
+
+    L = synth.make_config("32v")
+    say("[determinism] 32v select + sparse twice")
+    inputs = device_inputs(L)
+    a, da = gpu_select(L, inputs)
+    b, db = gpu_select(L, inputs)
+    for n in ("kept_count", "kept_idx", "drift", "key", "prob"):
+        assert np.array_equal(a[n], b[n]), n
+    q, k, v, _ = inputs
+    o1 = ress.ress_sparse_attn(q, k, v, da["kept_count"], da["kept_idx"], bq=L.bq, bk=L.bk)
+    o2 = ress.ress_sparse_attn(q, k, v, db["kept_count"], db["kept_idx"], bq=L.bq, bk=L.bk)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+
+
+def test_kept_list_edge_entries(ress):
+    """Empty lists give zero rows; entries outside [0, n_kb) are ignored; counts
+    above n_kb are clamped."""
+    import torch
+
+    L = small("ragged128x64")
+    say("[edges] empty / out-of-range kept lists")
+    q, k, v, _ = device_inputs(L)
+    n_qb, n_kb = L.n_qb, L.n_kb
+    kc = np.zeros((L.H, n_qb), np.int32)
+    ki = np.full((L.H, n_qb, n_kb), -1, np.int32)
+    kc[0, 0] = 3
+    ki[0, 0, :3] = [2, n_kb + 5, 0]  # one invalid entry
+    kc[1, :] = n_kb + 10  # clamped to n_kb: every block
+    ki[1, :, :] = np.arange(n_kb)[None, :]
+    kc[2, 1] = 1
+    ki[2, 1, 0] = -7  # only an invalid entry: no keys
+    dkc, dki = torch.from_numpy(kc).cuda(), torch.from_numpy(ki).cuda()
+    o = ress.ress_sparse_attn(q, k, v, dkc, dki, bq=L.bq, bk=L.bk).float().cpu().numpy()
+    assert np.all(o[0, L.bq:] == 0) and np.all(o[2, :L.bq] == 0) and np.all(o[2, L.bq:2 * L.bq] == 0)
+    ref_kc = kc.copy()
+    ref_ki = ki.copy()
+    ref_kc[0, 0] = 2
+    ref_ki[0, 0, :2] = [0, 2]
+    ref_kc[1, :] = n_kb
+    hs, ts = _all_tokens(L)
+    sel = (hs == 1) | ((hs == 0) & (ts < L.bq))
+    ref = __import__("oracle").attn_tokens(L.q, L.k, L.v, N=L.N, bq=L.bq, bk=L.bk, scale=1 / math.sqrt(64),
+                                           sel_h=hs[sel], sel_t=ts[sel], kept_count=ref_kc, kept_idx=ref_ki)
+    err = np.abs(o[hs[sel], ts[sel]] - ref)
+    assert err.max() <= 2e-2 and err.mean() <= 2e-3
+
+
+def test_errors_leave_outputs_untouched(ress):
+    import torch
+
+    L = small("forced64")
+    say("[errors] invalid budget: nothing written")
+    q, k, v, gram = device_inputs(L)
+    kc = torch.full((L.H, L.n_qb), 1234, dtype=torch.int32, device="cuda")
+    ki = torch.full((L.H, L.n_qb, L.n_kb), 1234, dtype=torch.int32, device="cuda")
+    bad = L.budgets.copy()
+    bad[1] = L.n_kb  # more than the candidates
+    with pytest.raises(ress.RessError) as e:
+        ress.ress_select(q, k, v, gram, bad, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                         kept_count=kc, kept_idx=ki)
+    assert e.value.status == ress.RESS_E_INVALID_ARG
+    ws = torch.empty(64, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ress.RessError) as e:
+        ress.ress_select(q, k, v, gram, L.budgets, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                         kept_count=kc, kept_idx=ki, workspace=ws)
+    assert e.value.status == ress.RESS_E_WORKSPACE
+    torch.cuda.synchronize()
+    assert bool(torch.all(kc == 1234)) and bool(torch.all(ki == 1234))
+
+
+def test_empty_shapes_are_no_ops(ress):
+    import torch
+
+    say("[edges] H = 0 and N = 0")
+    for H, N in ((0, 256), (2, 0)):
+        z = torch.zeros((H, N, 64), dtype=torch.bfloat16, device="cuda")
+        o = ress.ress_dense_attn(z, z.clone(), z.clone(), bq=64, bk=64)
+        assert o.shape == (H, N, 64)
+        g = torch.zeros((H, 64, 64), dtype=torch.float32, device="cuda")
+        out = ress.ress_select(z, z.clone(), z.clone(), g, np.zeros(H, np.int32), bq=64, bk=64)
+        assert out["kept_count"].numel() == 0
+    torch.cuda.synchronize()
+
+
+def test_key_block_cap(ress):
+    """n_kb = 4096 (the register-row cap) works; sampled rows against the oracle."""
+    L = synth.make_layer(4096 * 128 // 1374 + 1, 1369, 5, H=1, block=128, sparsity=0.9, seed=31, name="cap")
+    if L.n_kb > 4096:  # trim to exactly 4096 blocks
+        N = 4096 * 128
+        cut = L.N - N  # drop leading patch tokens; the special tail stays
+        L = synth.Layer(H=1, N=N, D=64, bq=128, bk=128, n_special_tail=L.n_special_tail,
+                        q=np.ascontiguousarray(L.q[:, cut:]), k=np.ascontiguousarray(L.k[:, cut:]),
+                        v=np.ascontiguousarray(L.v[:, cut:]), gram=L.gram,
+                        budgets=synth.budgets_from_sparsity([0.9], N, 128, L.n_special_tail),
+                        sparsity=np.array([0.9]), seed=31, name="cap")
+    assert L.n_kb == 4096
+    rows = np.array([0, 1, 2047, 4093, 4094, 4095])
+    say(f"[cap] n_kb={L.n_kb} budgets={L.budgets.tolist()} rows={rows.tolist()}")
+    gpu, _ = gpu_select(L, rounds=5)
+    ref = oracle_select(L, rounds=5, rows=rows)
+    compare_select(L, gpu, ref, rows=rows, label="n_kb=4096")
