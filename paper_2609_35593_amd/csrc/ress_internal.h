@@ -5,7 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/ress.h"
+#include "ress.h"
 
 namespace ress {
 
@@ -33,6 +33,7 @@ struct SelectParams {
     int first_forced;    // key blocks j >= first_forced are always kept (n_kb if none)
     int first_dense_qb;  // query blocks i >= first_dense_qb keep every block (n_qb if none)
     int rounds, swap_floor;
+    int items_per_xcd;   // (head, row group) items per XCD, set by the launcher
     double rho, eps;
     Pooled pooled;
     const float *gram;

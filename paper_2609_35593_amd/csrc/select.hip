@@ -3,17 +3,17 @@
 // rounds with track-best, and compaction of the kept-block lists.
 //
 // Work layout. A workgroup holds 4 independent waves; each wave owns R query
-// blocks ("rows") of one head, so loads of the head's pooled key/value tensors
-// are shared by the R rows in registers and by the 4 waves through L1.
+// blocks ("rows") of one head, so every load of the head's pooled key/value
+// tensors is used by the R rows in registers and by the 4 waves through L1.
 //  - Per-candidate quantities live "lane <-> key block": lane l, slot c holds key
-//    block j = l + 64 c (CPL slots). Channel-major copies of the pooled tensors
-//    make these passes coalesced.
-//  - Per-row vectors (vbar, M vbar, g, M g) live "lane <-> channel" (D = 64 is
-//    the wave width); values are broadcast with readlane.
+//    block j = l + 64 c (CPL slots).
+//  - Per-row vectors (Qbar, vbar, M vbar, g, M g) live "lane <-> channel"
+//    (D = 64 is the wave width) and are broadcast to the candidate lanes through
+//    the wave's LDS area, two doubles per read.
 //  - Every top-k is exact: a bitwise search for the k-th largest of
 //    order-preserving 64-bit keys, using wave ballots and popcounts, ties broken
-//    by the lower block index. No atomics, no data-dependent reduction order:
-//    reruns are bit-identical.
+//    by the lower block index. No atomics and no data-dependent reduction
+//    order: reruns are bit-identical.
 // All arithmetic is float64: CDNA4 runs float64 FMA at the rate of unpacked
 // float32, and it keeps the discrete decisions stable.
 #include <math.h>
@@ -24,14 +24,7 @@ namespace ress {
 namespace {
 
 constexpr int kThreads = 256;
-
-__device__ __forceinline__ double readlane_f64(double x, int l)
-{
-    const long long u = __double_as_longlong(x);
-    const int lo = __builtin_amdgcn_readlane((int)u, l);
-    const int hi = __builtin_amdgcn_readlane((int)(u >> 32), l);
-    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
-}
+constexpr int kWaves = kThreads / 64;
 
 __device__ __forceinline__ double wave_sum(double x)
 {
@@ -55,11 +48,13 @@ __device__ __forceinline__ unsigned long long order_key(double x)
     return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-// Exact top-k of the member slots by (key desc, block index asc). Returns this
-// lane's chosen slots as a bit mask. Requires 0 <= k <= number of members.
+// Exact top-k of the member slots by (key desc, block index asc). memb[c] is the
+// wave-wide mask of member lanes of slot c. Returns this lane's chosen slots as
+// a bit mask. Requires 0 <= k <= number of members.
 template <int CPL>
 __device__ unsigned long long topk_slots(const unsigned long long (&key)[CPL],
-                                         unsigned long long memb, int k, unsigned long long lane_lt)
+                                         const unsigned long long (&memb)[CPL], int k,
+                                         unsigned long long lane_bit, unsigned long long lane_lt)
 {
     if (k <= 0) return 0ull;
     unsigned long long thr = 0;  // invariant: #members with key >= thr is >= k
@@ -68,7 +63,7 @@ __device__ unsigned long long topk_slots(const unsigned long long (&key)[CPL],
         const unsigned long long cand = thr | (1ull << b);
         int cnt = 0;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) cnt += __popcll(__ballot(((memb >> c) & 1ull) && key[c] >= cand));
+        for (int c = 0; c < CPL; ++c) cnt += __popcll(__ballot(key[c] >= cand) & memb[c]);
         if (cnt >= k) {
             thr = cand;
             if (cnt == k) {  // exactly k keys reach thr: they are the top k
@@ -81,22 +76,20 @@ __device__ unsigned long long topk_slots(const unsigned long long (&key)[CPL],
     if (exact) {
 #pragma unroll
         for (int c = 0; c < CPL; ++c)
-            if (((memb >> c) & 1ull) && key[c] >= thr) chosen |= 1ull << c;
+            if ((memb[c] & lane_bit) && key[c] >= thr) chosen |= 1ull << c;
         return chosen;
     }
     // thr is the k-th largest key; take all larger ones and the lowest-index ties.
     int gt = 0;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) gt += __popcll(__ballot(((memb >> c) & 1ull) && key[c] > thr));
+    for (int c = 0; c < CPL; ++c) gt += __popcll(__ballot(key[c] > thr) & memb[c]);
     const int need = k - gt;
     int before = 0;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
-        const bool m = (memb >> c) & 1ull;
-        const bool tie = m && key[c] == thr;
-        const unsigned long long tb = __ballot(tie);
+        const unsigned long long tb = __ballot(key[c] == thr) & memb[c];
         const int rank = before + __popcll(tb & lane_lt);
-        if (m && (key[c] > thr || (tie && rank < need))) chosen |= 1ull << c;
+        if ((memb[c] & lane_bit) && (key[c] > thr || ((tb & lane_bit) && rank < need))) chosen |= 1ull << c;
         before += __popcll(tb);
     }
     return chosen;
@@ -109,29 +102,99 @@ __device__ __forceinline__ int swaps_of_round(int c, double rho, int r, int swap
     return m > swap_floor ? m : swap_floor;
 }
 
-// x = M_h y for a lane <-> channel vector y (M row-major, staged in LDS).
-__device__ __forceinline__ double mat_vec(const float *Ms, double y, int lane)
+// Per-wave LDS area (doubles): broadcast vectors vec[slot][R][64], one slot of
+// block weights wts[R][64], and a swap list of up to 64 (block, weight) pairs.
+template <int R>
+struct WaveLds {
+    static constexpr int kVecs = 3;  // 0: Qbar then vbar, 1: M vbar then M g, 2: g
+    static constexpr int kDoubles = kVecs * R * kD + R * 64 + 64 + 32;
+    double *base;
+    __device__ double *vec(int slot, int r) const { return base + (slot * R + r) * kD; }
+    __device__ double *wts(int r) const { return base + kVecs * R * kD + r * 64; }
+    __device__ double *swap_w() const { return base + kVecs * R * kD + R * 64; }
+    __device__ int *swap_j() const { return reinterpret_cast<int *>(base + kVecs * R * kD + R * 64 + 64); }
+};
+
+// x_r = M_h y_r for the R rows (lane <-> channel), M row-major in LDS (padded
+// rows), y_r broadcast from LDS two channels at a time.
+template <int R>
+__device__ __forceinline__ void mat_vec(const float *Ms, double *const (&y)[R], double (&x)[R], int lane)
 {
-    double acc = 0.0;
-    for (int b = 0; b < kD; ++b) acc = fma((double)Ms[lane * (kD + 1) + b], readlane_f64(y, b), acc);
-    return acc;
+#pragma unroll
+    for (int r = 0; r < R; ++r) x[r] = 0.0;
+#pragma unroll 4
+    for (int b = 0; b < kD; b += 2) {
+        const double m0 = (double)Ms[lane * (kD + 1) + b], m1 = (double)Ms[lane * (kD + 1) + b + 1];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const double2 yb = *reinterpret_cast<const double2 *>(y[r] + b);
+            x[r] = fma(m1, yb.y, fma(m0, yb.x, x[r]));
+        }
+    }
+}
+
+// Pass over the head's key blocks, lane <-> channel, with per-row block weights
+// w_r(j) held by the lane owning block j (slot c):
+//   SUB: out_r = sum_j w_r(j) (x_r - Vbar_j)      (net drift g, Eq. 10)
+//  !SUB: out_r = sum_j w_r(j) Vbar_j              (dense pooled output, Eq. 1)
+// in ascending block order with eight rows of Vbar in flight; the weights of one
+// slot (64 blocks) at a time are staged in the wave's LDS area.
+template <int CPL, int R, bool SUB>
+__device__ __forceinline__ void block_pass(const WaveLds<R> &lds, const double (&w)[R][CPL], const double (&x)[R],
+                                           const double *__restrict__ Vr, int nkb, int lane, double (&out)[R])
+{
+#pragma unroll
+    for (int r = 0; r < R; ++r) out[r] = 0.0;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int r = 0; r < R; ++r) lds.wts(r)[lane] = w[r][c];  // 0 past the last block
+        __builtin_amdgcn_wave_barrier();
+        const int lim = min(64, nkb - 64 * c);
+        const double *vrow = Vr + (size_t)64 * c * kD;
+        for (int l0 = 0; l0 < lim; l0 += 8) {
+            double vj[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) vj[u] = vrow[(size_t)min(l0 + u, lim - 1) * kD + lane];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const double *wr = lds.wts(r) + l0;
+#pragma unroll
+                for (int u = 0; u < 8; u += 2) {
+                    const double2 pw = *reinterpret_cast<const double2 *>(wr + u);
+                    if (SUB)
+                        out[r] = fma(pw.y, x[r] - vj[u + 1], fma(pw.x, x[r] - vj[u], out[r]));
+                    else
+                        out[r] = fma(pw.y, vj[u + 1], fma(pw.x, vj[u], out[r]));
+                }
+            }
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
 }
 
 template <int CPL, int R>
 __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
 {
+    __shared__ double smem[kWaves * WaveLds<R>::kDoubles];
     __shared__ float Ms[kD * (kD + 1)];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const unsigned long long lane_lt = (1ull << lane) - 1ull;
-    const int groups = (p.n_qb + 4 * R - 1) / (4 * R);
-    const int h = blockIdx.x / groups;
-    const int row0 = (blockIdx.x % groups) * 4 * R + wave * R;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const unsigned long long lane_bit = 1ull << lane, lane_lt = lane_bit - 1ull;
+    // Workgroups are numbered so that each of the 8 XCDs gets a contiguous range
+    // of (head, row group) items: the rows of a head share one XCD's L2.
+    const int groups = (p.n_qb + kWaves * R - 1) / (kWaves * R);
+    const int item = (blockIdx.x & 7) * p.items_per_xcd + (blockIdx.x >> 3);
+    if (item >= p.H * groups) return;
+    const int h = item / groups;
+    const int row0 = (item % groups) * kWaves * R + wave * R;
     {
         const float *Mh = p.gram + (size_t)h * kD * kD;
-        for (int e = threadIdx.x; e < kD * kD; e += kThreads) Ms[(e >> 6) * (kD + 1) + (e & 63)] = Mh[e];
+        for (int e = tid; e < kD * kD; e += kThreads) Ms[(e >> 6) * (kD + 1) + (e & 63)] = Mh[e];
     }
     __syncthreads();
-    if (row0 >= p.n_qb) return;
+    if (row0 >= p.n_qb) return;  // waves are independent from here on
+    const WaveLds<R> lds{smem + wave * WaveLds<R>::kDoubles};
 
     const int nkb = p.n_kb, nqb = p.n_qb;
     const double eps = p.eps;
@@ -139,41 +202,49 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
     const double *Vr = p.pooled.vbar + (size_t)h * nkb * kD;
     const double *Vt = p.pooled.vbarT + (size_t)h * kD * nkb;
     const double *Ut = p.pooled.uT + (size_t)h * kD * nkb;
-    const double *Qb = p.pooled.qbar + (size_t)h * nqb * kD;
     const int c_h = p.budgets[h];
     const int n_p = p.first_forced;  // candidates are the key blocks j < first_forced
 
     int irow[R];
     bool live[R], dense[R];
+    double *vbv[R], *wvv[R], *gv[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         live[r] = row0 + r < nqb;
         irow[r] = live[r] ? row0 + r : nqb - 1;
         dense[r] = irow[r] >= p.first_dense_qb || c_h >= n_p;
+        vbv[r] = lds.vec(0, r);
+        wvv[r] = lds.vec(1, r);
+        gv[r] = lds.vec(2, r);
+        vbv[r][lane] = p.pooled.qbar[((size_t)h * nqb + irow[r]) * kD + lane];  // Qbar_i for now
     }
-    unsigned long long memb = 0;  // candidate slots of this lane
+    int jc[CPL];  // this lane's key block per slot, clamped into range for loads
+    bool valid[CPL];
+    unsigned long long memb[CPL];  // wave masks of candidate lanes per slot
 #pragma unroll
-    for (int c = 0; c < CPL; ++c)
-        if (lane + 64 * c < n_p) memb |= 1ull << c;
+    for (int c = 0; c < CPL; ++c) {
+        const int j = lane + 64 * c;
+        valid[c] = j < nkb;
+        jc[c] = valid[c] ? j : nkb - 1;
+        memb[c] = __ballot(j < n_p);
+    }
+    __builtin_amdgcn_wave_barrier();
 
     // Pooled logits Qbar_i . Kbar_j / sqrt(D) (Eq. 1).
     double acc[R][CPL], P[R][CPL], S2[R][CPL];
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+    for (int c = 0; c < CPL; ++c) {
+        const double *col = Kt + jc[c];
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
-    for (int d = 0; d < kD; ++d) {
-        double kd[CPL];
+        for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
+#pragma unroll 4
+        for (int d = 0; d < kD; d += 2) {
+            const double k0 = col[(size_t)d * nkb], k1 = col[(size_t)(d + 1) * nkb];
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            const int j = lane + 64 * c;
-            kd[c] = j < nkb ? Kt[(size_t)d * nkb + j] : 0.0;
-        }
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const double qd = Qb[(size_t)irow[r] * kD + d];
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) acc[r][c] = fma(qd, kd[c], acc[r][c]);
+            for (int r = 0; r < R; ++r) {
+                const double2 qd = *reinterpret_cast<const double2 *>(vbv[r] + d);
+                acc[r][c] = fma(qd.y, k1, fma(qd.x, k0, acc[r][c]));
+            }
         }
     }
     // Softmax over all key blocks.
@@ -183,13 +254,13 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
             acc[r][c] *= 0.125;  // 1/sqrt(64)
-            if (lane + 64 * c < nkb) mx = fmax(mx, acc[r][c]);
+            if (valid[c]) mx = fmax(mx, acc[r][c]);
         }
         mx = wave_max(mx);
         double z = 0.0;
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-            P[r][c] = lane + 64 * c < nkb ? exp(acc[r][c] - mx) : 0.0;
+            P[r][c] = valid[c] ? exp(acc[r][c] - mx) : 0.0;
             z += P[r][c];
         }
         z = wave_sum(z);
@@ -199,45 +270,40 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
             double *po = p.prob_out + ((size_t)h * nqb + irow[r]) * nkb;
 #pragma unroll
             for (int c = 0; c < CPL; ++c)
-                if (lane + 64 * c < nkb) po[lane + 64 * c] = P[r][c];
+                if (valid[c]) po[lane + 64 * c] = P[r][c];
         }
     }
 
-    // Dense pooled output vbar_i = sum_j P_ij Vbar_j (lane <-> channel) and M vbar_i.
-    double vb[R], wv[R];
+    // Dense pooled output vbar_i = sum_j P_ij Vbar_j and M vbar_i (lane <-> channel).
+    {
+        double vb[R], wv[R];
+        block_pass<CPL, R, false>(lds, P, vb, Vr, nkb, lane, vb);
 #pragma unroll
-    for (int r = 0; r < R; ++r) vb[r] = 0.0;
+        for (int r = 0; r < R; ++r) vbv[r][lane] = vb[r];
+        __builtin_amdgcn_wave_barrier();
+        mat_vec<R>(Ms, vbv, wv, lane);
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-        const int lim = min(64, nkb - 64 * c);
-        for (int l2 = 0; l2 < lim; ++l2) {
-            const double vjd = Vr[(size_t)(64 * c + l2) * kD + lane];
-#pragma unroll
-            for (int r = 0; r < R; ++r) vb[r] = fma(readlane_f64(P[r][c], l2), vjd, vb[r]);
-        }
+        for (int r = 0; r < R; ++r) wvv[r][lane] = wv[r];
+        __builtin_amdgcn_wave_barrier();
     }
-#pragma unroll
-    for (int r = 0; r < R; ++r) wv[r] = mat_vec(Ms, vb[r], lane);
 
     // q_ij = e^T M e with e = vbar_i - Vbar_j, as e . (M vbar_i - M Vbar_j) (Eq. 9);
     // s_ij = P_ij sqrt(q_ij), key_ij = s_ij / max(1 - P_ij, eps) (Eqs. 6-7).
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+    for (int c = 0; c < CPL; ++c) {
+        const double *vcol = Vt + jc[c], *ucol = Ut + jc[c];
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
-    for (int d = 0; d < kD; ++d) {
-        double vt[CPL], ut[CPL];
+        for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
+#pragma unroll 4
+        for (int d = 0; d < kD; d += 2) {
+            const double v0 = vcol[(size_t)d * nkb], v1 = vcol[(size_t)(d + 1) * nkb];
+            const double u0 = ucol[(size_t)d * nkb], u1 = ucol[(size_t)(d + 1) * nkb];
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            const int j = lane + 64 * c;
-            vt[c] = j < nkb ? Vt[(size_t)d * nkb + j] : 0.0;
-            ut[c] = j < nkb ? Ut[(size_t)d * nkb + j] : 0.0;
-        }
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const double vbd = readlane_f64(vb[r], d), wd = readlane_f64(wv[r], d);
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) acc[r][c] = fma(vbd - vt[c], wd - ut[c], acc[r][c]);
+            for (int r = 0; r < R; ++r) {
+                const double2 vb = *reinterpret_cast<const double2 *>(vbv[r] + d);
+                const double2 wd = *reinterpret_cast<const double2 *>(wvv[r] + d);
+                acc[r][c] = fma(vb.y - v1, wd.y - u1, fma(vb.x - v0, wd.x - u0, acc[r][c]));
+            }
         }
     }
 #pragma unroll
@@ -255,130 +321,153 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
 #pragma unroll
             for (int c = 0; c < CPL; ++c) {
                 const int j = lane + 64 * c;
-                if (j < nkb) ko[j] = j < n_p ? acc[r][c] : -1.0;
+                if (valid[c]) ko[j] = j < n_p ? acc[r][c] : -1.0;
             }
         }
     }
 
-    // Initial selection (Eq. 7) and the state of its drop set (Eqs. 10-12).
+    // Initial selection (Eq. 7), then the state of each drop set (Eqs. 10-12):
+    // g = sum_{j in D} P_j (vbar - Vbar_j), K = 1 - sum_{j in D} P_j, G = g^T M g.
     unsigned long long inD[R], best[R];
-    double K[R], G[R], J[R], J0[R], Jb[R], gd[R], hd[R];
+    double K[R], G[R], J[R], J0[R], Jb[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        inD[r] = best[r] = 0ull;
-        K[r] = 1.0;
-        G[r] = J[r] = J0[r] = Jb[r] = gd[r] = hd[r] = 0.0;
-        if (dense[r]) continue;
-        unsigned long long ko[CPL];
+        inD[r] = 0ull;
+        if (!dense[r]) {
+            unsigned long long ko[CPL];
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) ko[c] = order_key(acc[r][c]);
-        inD[r] = memb & ~topk_slots<CPL>(ko, memb, c_h, lane_lt);
+            for (int c = 0; c < CPL; ++c) ko[c] = order_key(acc[r][c]);
+            const unsigned long long keep = topk_slots<CPL>(ko, memb, c_h, lane_bit, lane_lt);
+#pragma unroll
+            for (int c = 0; c < CPL; ++c)
+                if ((memb[c] & lane_bit) && !((keep >> c) & 1ull)) inD[r] |= 1ull << c;
+        }
         double mass = 0.0;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c)
-            if ((inD[r] >> c) & 1ull) mass += P[r][c];
-        K[r] = 1.0 - wave_sum(mass);
-        double g = 0.0;
-#pragma unroll
         for (int c = 0; c < CPL; ++c) {
-            unsigned long long bm = __ballot((inD[r] >> c) & 1ull);
-            while (bm) {
-                const int b = __ffsll((long long)bm) - 1;
-                bm &= bm - 1ull;
-                const double pj = readlane_f64(P[r][c], b);
-                g = fma(pj, vb[r] - Vr[(size_t)(64 * c + b) * kD + lane], g);
-            }
+            acc[r][c] = ((inD[r] >> c) & 1ull) ? P[r][c] : 0.0;  // weights of the g pass
+            mass += acc[r][c];
         }
-        gd[r] = g;
-        hd[r] = mat_vec(Ms, g, lane);
-        G[r] = wave_sum(g * hd[r]);
-        const double Kh = K[r] > eps ? K[r] : eps;
-        J[r] = J0[r] = Jb[r] = G[r] / (Kh * Kh);
+        K[r] = 1.0 - wave_sum(mass);
+    }
+    {
+        double vb[R], g[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) vb[r] = vbv[r][lane];
+        block_pass<CPL, R, true>(lds, acc, vb, Vr, nkb, lane, g);
+#pragma unroll
+        for (int r = 0; r < R; ++r) gv[r][lane] = g[r];
+    }
+    double *hv[R];  // M g reuses the slot of M vbar
+#pragma unroll
+    for (int r = 0; r < R; ++r) hv[r] = wvv[r];
+    auto objective = [&]() {  // h = M g, G = g . h, J = G / max(K, eps)^2
+        __builtin_amdgcn_wave_barrier();
+        double hh[R];
+        mat_vec<R>(Ms, gv, hh, lane);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            hv[r][lane] = hh[r];
+            G[r] = wave_sum(gv[r][lane] * hh[r]);
+            const double Kh = K[r] > eps ? K[r] : eps;
+            J[r] = G[r] / (Kh * Kh);
+        }
+        __builtin_amdgcn_wave_barrier();
+    };
+    objective();
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        J0[r] = Jb[r] = J[r];
         best[r] = inD[r];
     }
 
     // Budget-neutral restoration rounds (Eqs. 13-17) with track-best.
     const int nD = n_p - c_h, nS = c_h;
+    double *swap_w = lds.swap_w();
+    int *swap_j = lds.swap_j();
     for (int rr = 0; rr < p.rounds; ++rr) {
         int m = swaps_of_round(c_h, p.rho, rr, p.swap_floor);
         m = min(m, min(nD, nS));
         if (m <= 0) break;
-        // e_k . (M g) for every candidate k of every row (shares the loads).
+        // e_k . (M g) for every candidate k of every row.
 #pragma unroll
-        for (int r = 0; r < R; ++r)
+        for (int c = 0; c < CPL; ++c) {
+            const double *vcol = Vt + jc[c];
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
-        for (int d = 0; d < kD; ++d) {
-            double vt[CPL];
+            for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
+#pragma unroll 4
+            for (int d = 0; d < kD; d += 2) {
+                const double v0 = vcol[(size_t)d * nkb], v1 = vcol[(size_t)(d + 1) * nkb];
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                const int j = lane + 64 * c;
-                vt[c] = j < nkb ? Vt[(size_t)d * nkb + j] : 0.0;
-            }
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const double vbd = readlane_f64(vb[r], d), hdd = readlane_f64(hd[r], d);
-#pragma unroll
-                for (int c = 0; c < CPL; ++c) acc[r][c] = fma(vbd - vt[c], hdd, acc[r][c]);
+                for (int r = 0; r < R; ++r) {
+                    const double2 vb = *reinterpret_cast<const double2 *>(vbv[r] + d);
+                    const double2 hd = *reinterpret_cast<const double2 *>(hv[r] + d);
+                    acc[r][c] = fma(vb.y - v1, hd.y, fma(vb.x - v0, hd.x, acc[r][c]));
+                }
             }
         }
+        // Gains of every single restore / drop at the round-start state; the m best
+        // of each kind are applied together, g and K following Eq. 13.
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             if (dense[r]) continue;
-            unsigned long long dj[CPL];
+            unsigned long long dj[CPL], memD[CPL], memS[CPL];
 #pragma unroll
             for (int c = 0; c < CPL; ++c) {
+                const bool in = (inD[r] >> c) & 1ull;
                 const double dkMg = P[r][c] * acc[r][c];
-                double dG, u;
-                if ((inD[r] >> c) & 1ull) {  // restore: Eq. 14
-                    dG = -2.0 * dkMg + S2[r][c];
-                    u = P[r][c];
-                } else {  // drop: Eq. 15
-                    dG = 2.0 * dkMg + S2[r][c];
-                    u = -P[r][c];
-                }
-                const double Kn = K[r] + u;
+                const double dG = in ? -2.0 * dkMg + S2[r][c] : 2.0 * dkMg + S2[r][c];  // Eqs. 14-15
+                const double Kn = K[r] + (in ? P[r][c] : -P[r][c]);
                 const double Knh = Kn > eps ? Kn : eps;
                 dj[c] = order_key(J[r] - (G[r] + dG) / (Knh * Knh));  // Eq. 16
+                memD[c] = __ballot(in);
+                memS[c] = memb[c] & ~memD[c];
             }
-            const unsigned long long rest = topk_slots<CPL>(dj, inD[r], m, lane_lt);
-            const unsigned long long drop = topk_slots<CPL>(dj, memb & ~inD[r], m, lane_lt);
-            double mr = 0.0, md = 0.0;
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                if ((rest >> c) & 1ull) mr += P[r][c];
-                if ((drop >> c) & 1ull) md += P[r][c];
-            }
-            K[r] = (K[r] + wave_sum(mr)) - wave_sum(md);  // Eq. 13
-            double g = gd[r];
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                unsigned long long bm = __ballot((rest >> c) & 1ull);
-                while (bm) {
-                    const int b = __ffsll((long long)bm) - 1;
-                    bm &= bm - 1ull;
-                    const double pj = readlane_f64(P[r][c], b);
-                    g = fma(-pj, vb[r] - Vr[(size_t)(64 * c + b) * kD + lane], g);
-                }
-                bm = __ballot((drop >> c) & 1ull);
-                while (bm) {
-                    const int b = __ffsll((long long)bm) - 1;
-                    bm &= bm - 1ull;
-                    const double pj = readlane_f64(P[r][c], b);
-                    g = fma(pj, vb[r] - Vr[(size_t)(64 * c + b) * kD + lane], g);
-                }
-            }
-            gd[r] = g;
+            const unsigned long long rest = topk_slots<CPL>(dj, memD, m, lane_bit, lane_lt);
+            const unsigned long long drop = topk_slots<CPL>(dj, memS, m, lane_bit, lane_lt);
             inD[r] = (inD[r] & ~rest) | drop;
-            hd[r] = mat_vec(Ms, g, lane);
-            G[r] = wave_sum(g * hd[r]);
-            const double Kh = K[r] > eps ? K[r] : eps;
-            J[r] = G[r] / (Kh * Kh);
-            if (J[r] < Jb[r]) {
+            double mr = 0.0, md = 0.0;
+            double g = gv[r][lane];
+            const double vbl = vbv[r][lane];
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                // Compact this slot's swapped blocks: restores subtract d_k, drops add it.
+                const bool is_rest = (rest >> c) & 1ull, is_drop = (drop >> c) & 1ull;
+                const unsigned long long sm = __ballot(is_rest || is_drop);
+                if (sm == 0ull) continue;
+                __builtin_amdgcn_wave_barrier();
+                if (is_rest || is_drop) {
+                    const int pos = __popcll(sm & lane_lt);
+                    swap_j[pos] = lane + 64 * c;
+                    swap_w[pos] = is_drop ? P[r][c] : -P[r][c];
+                }
+                if (is_rest) mr += P[r][c];
+                if (is_drop) md += P[r][c];
+                __builtin_amdgcn_wave_barrier();
+                const int n = __popcll(sm);
+                for (int t0 = 0; t0 < n; t0 += 8) {
+                    double vj[8], wj[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int t = min(t0 + u, n - 1);
+                        vj[u] = Vr[(size_t)swap_j[t] * kD + lane];
+                        wj[u] = t0 + u < n ? swap_w[t] : 0.0;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) g = fma(wj[u], vbl - vj[u], g);
+                }
+            }
+            K[r] = (K[r] + wave_sum(mr)) - wave_sum(md);
+            __builtin_amdgcn_wave_barrier();
+            gv[r][lane] = g;
+        }
+        objective();
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            if (!dense[r] && J[r] < Jb[r]) {
                 Jb[r] = J[r];
                 best[r] = inD[r];
             }
-        }
     }
 
     // Kept lists: (P \ D_best) u F in ascending block order, padded with -1.
@@ -390,10 +479,9 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
         int before = 0;
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-            const int j = lane + 64 * c;
-            const bool kept = j < nkb && !((best[r] >> c) & 1ull);
+            const bool kept = valid[c] && !((best[r] >> c) & 1ull);
             const unsigned long long km = __ballot(kept);
-            if (kept) out[before + __popcll(km & lane_lt)] = j;
+            if (kept) out[before + __popcll(km & lane_lt)] = lane + 64 * c;
             before += __popcll(km);
         }
         for (int t = before + lane; t < nkb; t += 64) out[t] = -1;
@@ -410,8 +498,10 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
 template <int CPL, int R>
 hipError_t launch_cfg(const SelectParams &p, hipStream_t s)
 {
-    const int groups = (p.n_qb + 4 * R - 1) / (4 * R);
-    hipLaunchKernelGGL((select_kernel<CPL, R>), dim3((unsigned)(p.H * groups)), dim3(kThreads), 0, s, p);
+    SelectParams q = p;
+    const int groups = (p.n_qb + kWaves * R - 1) / (kWaves * R);
+    q.items_per_xcd = (p.H * groups + 7) / 8;
+    hipLaunchKernelGGL((select_kernel<CPL, R>), dim3((unsigned)(8 * q.items_per_xcd)), dim3(kThreads), 0, s, q);
     return hipGetLastError();
 }
 
@@ -424,10 +514,10 @@ hipError_t launch_select(const SelectParams &p, hipStream_t s)
     if (n <= 64) return launch_cfg<1, 4>(p, s);
     if (n <= 128) return launch_cfg<2, 4>(p, s);
     if (n <= 256) return launch_cfg<4, 4>(p, s);
-    if (n <= 384) return launch_cfg<6, 4>(p, s);
+    if (n <= 384) return launch_cfg<6, 2>(p, s);
     if (n <= 512) return launch_cfg<8, 2>(p, s);
     if (n <= 768) return launch_cfg<12, 2>(p, s);
-    if (n <= 1088) return launch_cfg<17, 2>(p, s);
+    if (n <= 1088) return launch_cfg<17, 1>(p, s);
     if (n <= 1536) return launch_cfg<24, 1>(p, s);
     if (n <= 2048) return launch_cfg<32, 1>(p, s);
     if (n <= 3072) return launch_cfg<48, 1>(p, s);
