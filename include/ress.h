@@ -37,7 +37,7 @@ extern "C" {
 /* Status codes. */
 #define RESS_OK 0
 #define RESS_E_INVALID_ARG (-1) /* null pointer, negative size, bad parameter or budget */
-#define RESS_E_UNSUPPORTED (-2) /* D != 64, block size not 64/128, n_kb > 4096, H > 256 */
+#define RESS_E_UNSUPPORTED (-2) /* D != 64, block size not 64/128, n_kb > 4096, H > 256, N > 2^24 */
 #define RESS_E_WORKSPACE (-3)   /* workspace missing, too small or misaligned */
 #define RESS_E_HIP (-4)         /* a HIP launch call failed */
 
@@ -46,10 +46,12 @@ extern "C" {
 #define RESS_MAX_KEY_BLOCKS 4096
 #define RESS_MAX_HEADS 256
 #define RESS_MAX_ROUNDS 32
+/* Largest N accepted by every entry point (token offsets within a head stay in 32 bits). */
+#define RESS_MAX_TOKENS (1 << 24)
 
 typedef struct {
     int H;              /* heads, 0..RESS_MAX_HEADS */
-    int N;              /* tokens per head (all views concatenated), >= 0 */
+    int N;              /* tokens per head (all views concatenated), 0..RESS_MAX_TOKENS */
     int D;              /* head dimension; must be 64 */
     int bq;             /* query block size: 64 or 128 */
     int bk;             /* key block size: 64 or 128 */

@@ -5,18 +5,34 @@
 // One workgroup per (head, query block), BQ/32 waves, each wave owning 32 query
 // rows. The score tile is computed transposed, S^T = K Q^T, with
 // v_mfma_f32_32x32x16_bf16: its accumulator puts one query per lane (lane l and
-// l+32 share query l%32, each holding 16 of every 32 keys), so the row max and
-// row sum stay in the lane except for one exchange with lane l^32, and the
-// probabilities already sit in the B-operand layout of O^T = V^T P^T. V is
-// stored transposed in LDS with its keys permuted inside each group of 16 to
-// match that layout. K rows and V^T rows are XOR-swizzled in 16-byte chunks so
-// that the MFMA operand reads and the tile writes are free of bank conflicts.
+// l+32 share query l%32, each holding 16 of every 32 keys), so row sums stay in
+// the lane except for one exchange with lane l^32, and the probabilities already
+// sit in the B-operand layout of O^T = V^T P^T.
 //
-// Softmax details: exponentials in base 2 with the scale folded in; row sums are
-// taken on the bf16-rounded probabilities (the values the PV product uses) with
-// packed bf16 dot products; the running maximum is only raised, and O rescaled,
-// when some row's maximum grows by more than 2^8, so probabilities stay below
-// 256 and most tiles skip the rescale.
+// Keys are consumed in 128-key tiles (one 128-key block, or two 64-key blocks
+// of the list) split into 64-key halves, software-pipelined over halves: the
+// step that forms the probabilities of half n also issues the score MFMAs of
+// half n+1 and the PV MFMAs of half n-1, so one basic block holds 16 MFMAs next
+// to the softmax arithmetic and the matrix and vector pipes run side by side.
+// K and V tiles move from global memory straight into LDS (global_load_lds, 16
+// bytes per lane, 1 KB per wave instruction) in two-slot rings; one barrier per
+// tile, between its two halves, both publishes the tiles loaded one tile earlier
+// and frees the slots the next loads overwrite (K of tile t+2, V of tile t+1).
+// Tiles stay row-major (64 channels = 128 bytes per key) with their 16-byte
+// chunks XOR-swizzled per key; the swizzle is applied by choosing each lane's
+// source chunk, since a DMA instruction fills LDS contiguously. The V^T operand
+// comes from ds_read_b64_tr_b16: within 16 lanes, lane s points at 4 channels
+// of key k0 + s/4 and lane i receives channel d0 + i of keys k0..k0+3, which is
+// the transpose the PV product needs.
+//
+// Softmax: base-2 exponentials with the scale folded into one FMA; row sums over
+// the bf16-rounded probabilities (the values the PV product consumes) with
+// packed bf16 dot products. There is no per-half maximum: each row keeps a
+// reference maximum (the largest score seen when it was last set) and forms the
+// probabilities against it directly; only when a half's probability sum leaves
+// [0, 2^20] (a score above the reference by more than 2^20 in probability, or
+// the first keys of the row) is the half redone with its true maximum and O
+// rescaled. Softmax is invariant to the reference, so this changes rounding only.
 //
 // Workgroups are numbered so that the 8 XCDs each receive a contiguous range of
 // (head, query block) items: neighbouring query blocks of a head share an XCD
@@ -28,49 +44,42 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef __bf16 bf16x2 __attribute__((__vector_size__(2 * sizeof(__bf16))));
+typedef short s16x4 __attribute__((__vector_size__(4 * sizeof(short))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr float kRescaleLog2 = 8.0f;  // lazy-rescale threshold, in powers of two
+constexpr float kSumLimit = 1048576.0f;  // 2^20: largest probability sum a half may reach
 
 __device__ __forceinline__ unsigned int bf16_bits(float x)
 {
     return (unsigned int)__builtin_bit_cast(unsigned short, (__bf16)x);
 }
 
-// Position of key kk (0..15) inside its 16-key group of the V^T tile: bits 2 and
-// 3 swapped, so that lane half hh reads the 8 keys it holds probabilities for.
-__device__ __forceinline__ int vt_pos(int kk) { return (kk & 3) | ((kk & 4) << 1) | ((kk & 8) >> 1); }
+// XOR applied to the 16-byte chunk index of LDS row `row` (K and V tiles, 128-byte
+// rows, two rows per 256-byte bank row). With s = swz(row):
+//  - 16 consecutive rows read at one logical chunk (score operand, 16 lanes x 16 B)
+//    land on 16 distinct (bank half, chunk) pairs, since (row>>1)&7 -> s is a bijection;
+//  - the transpose reads (32 lanes x 8 B: keys 8n..8n+3 or 8n+4..8n+7, each at the 4
+//    chunks of one 32-channel half) are split by bit 2 of s between rows 8n and 8n+2.
+__device__ __forceinline__ int swz(int row) { return (((row >> 1) & 1) << 2) | ((row >> 2) & 3); }
 
-// LDS swizzles (16-byte chunk index within a row). A 16-lane phase of a 16-byte
-// read and a 32-lane phase of an 8-byte write must hit distinct bank groups of a
-// 256-byte bank row.
-// K rows are 128 bytes: 16 consecutive rows read one logical chunk.
-__device__ __forceinline__ int k_chunk(int row, int ch) { return ch ^ ((row >> 1) & 7); }
-// V^T rows (one channel d, BK keys). With 128 keys (16 chunks): reads cover 16
-// consecutive channels, writes cover channels 8dc + e for dc = 0..7 and two
-// logical chunks; h(d) is a bijection on each 16 consecutive channels and its
-// bits 1..3 take 8 distinct values over dc. With 64 keys (8 chunks, two rows
-// per bank row) the reads are conflict-free.
-template <int BK>
-__device__ __forceinline__ int v_chunk(int d, int ch)
-{
-    if constexpr (BK == 128)
-        return ch ^ ((d & 15) ^ (((d >> 3) & 7) << 1));
-    else
-        return ch ^ ((d >> 1) & 7);
-}
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 template <int BQ, int BK, bool SPARSE>
 __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
 {
-    constexpr int T = BQ * 2;         // threads
-    constexpr int NT = BK / 32;       // 32-key sub-tiles per key block
-    constexpr int KU = BK * 8 / T;    // 16-byte K pieces per thread
-    constexpr int VUNITS = BK * 2;    // 4-key x 8-channel V pieces per tile
-    constexpr int VU = (VUNITS + T - 1) / T;
-    constexpr int VROW = BK * 2;      // bytes per V^T row
-    __shared__ __attribute__((aligned(16))) unsigned char k_lds[BK * 128];
-    __shared__ __attribute__((aligned(16))) unsigned char v_lds[kD * VROW];
+    constexpr int T = BQ * 2;                 // threads
+    constexpr int NW = BQ / 32;               // waves
+    constexpr int EPT = BK == 128 ? 1 : 2;    // kept-list entries per 128-key tile
+    constexpr int LPH = 64 * 8 / T;           // 16-byte DMA loads per thread, tensor and half
+    constexpr int TILE = 128 * 128;           // bytes of one K (or V) tile
+    constexpr int HALF = TILE / 2;
+    static_assert(64 * 8 % T == 0 && LPH >= 1, "a half tile must split evenly over the threads");
+    __shared__ __attribute__((aligned(1024))) unsigned char k_lds0[TILE];
+    __shared__ __attribute__((aligned(1024))) unsigned char k_lds1[TILE];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_lds0[TILE];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_lds1[TILE];
 
     const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
     const int item = xcd * p.items_per_xcd + local;
@@ -78,8 +87,10 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
     const int h = item / p.n_qb;
     const int i = p.n_qb - 1 - item % p.n_qb;  // last query blocks first (they may be dense)
     const int N = p.N, n_kb = p.n_kb;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hh = lane >> 5, ql = lane & 31;
+    const int g16 = (lane >> 4) & 1, s16 = lane & 15;
     const int q0 = i * BQ + wave * 32 + ql;
     const size_t head = (size_t)h * N;
 
@@ -92,80 +103,104 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
             qf[kk] = bf16x8{};
     }
 
-    int ntiles;
+    int n_ent;  // key blocks to visit
     const int32_t *list = nullptr;
     if constexpr (SPARSE) {
         const size_t row = (size_t)h * p.n_qb + i;
-        ntiles = min(max(p.kept_count[row], 0), n_kb);
+        n_ent = min(max(p.kept_count[row], 0), n_kb);
         list = p.kept_idx + row * n_kb;
     } else {
-        ntiles = n_kb;
+        n_ent = n_kb;
     }
+    const int L = (n_ent + EPT - 1) / EPT;  // 128-key tiles
 
-    uint4 kreg[KU];
-    uint4 vreg[VU][4];
-    auto tile_index = [&](int it) -> int {
-        if constexpr (SPARSE) return list[it];
-        else return it;
+    // Kept block indices, read 64 at a time: lane l of idx_lo holds entry 64c + l of
+    // the list, idx_hi the next 64, loaded one chunk ahead of use.
+    int idx_lo = -1, idx_hi = -1;
+    auto load_chunk = [&](int c) __attribute__((always_inline)) -> int {
+        const int t = 64 * c + lane;
+        return t < n_ent ? list[t] : -1;
     };
-    auto load_tile = [&](int j) {
-        const bool valid = j >= 0 && j < n_kb;
-        const size_t base = (size_t)(valid ? j : 0) * BK;
-#pragma unroll
-        for (int u = 0; u < KU; ++u) {
-            const int unit = tid + u * T, kr = unit >> 3, ch = unit & 7;
-            const size_t tok = base + kr;
-            kreg[u] = (valid && tok < (size_t)N)
-                          ? *reinterpret_cast<const uint4 *>(p.k + (head + tok) * kD + ch * 8)
-                          : make_uint4(0, 0, 0, 0);
+    if constexpr (SPARSE) {
+        idx_lo = load_chunk(0);
+        idx_hi = load_chunk(1);
+    }
+    // Block index of entry e (-1 past the end); called for e = 0, 1, 2, ... in order.
+    auto entry = [&](int e) __attribute__((always_inline)) -> int {
+        if constexpr (SPARSE) {
+            if (e > 0 && (e & 63) == 0) {
+                idx_lo = idx_hi;
+                idx_hi = load_chunk((e >> 6) + 1);
+            }
+            return __builtin_amdgcn_readlane(idx_lo, e & 63);
+        } else {
+            return e < n_ent ? e : -1;
         }
+    };
+    auto fetch_tile = [&](int t, int (&jt)[EPT]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int u = 0; u < VU; ++u) {
-            const int unit = tid + u * T, kg = unit >> 3, dc = unit & 7;
+        for (int e = 0; e < EPT; ++e) jt[e] = entry(t * EPT + e);
+    };
+    auto valid = [&](int j) __attribute__((always_inline)) { return j >= 0 && j < n_kb; };
+    // First token of half hf of a tile, and how many of its 64 keys are real.
+    auto half_row0 = [&](const int (&jt)[EPT], int hf) __attribute__((always_inline)) -> int {
+        if constexpr (EPT == 1) return valid(jt[0]) ? jt[0] * 128 + 64 * hf : 0;
+        else return valid(jt[hf]) ? jt[hf] * 64 : 0;
+    };
+    auto half_keys = [&](const int (&jt)[EPT], int hf) __attribute__((always_inline)) -> int {
+        if constexpr (EPT == 1) return valid(jt[0]) ? max(0, min(64, N - jt[0] * 128 - 64 * hf)) : 0;
+        else return valid(jt[hf]) ? min(64, N - jt[hf] * 64) : 0;
+    };
+
+    // DMA: thread-constant byte offsets within a 64-row half (row r of the half,
+    // the logical chunk that belongs at physical chunk lane&7).
+    const unsigned char *kbytes = reinterpret_cast<const unsigned char *>(p.k + head * kD);
+    const unsigned char *vbytes = reinterpret_cast<const unsigned char *>(p.v + head * kD);
+    unsigned int doff[LPH];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const size_t tok = base + kg * 4 + r;
-                vreg[u][r] = (unit < VUNITS && valid && tok < (size_t)N)
-                                 ? *reinterpret_cast<const uint4 *>(p.v + (head + tok) * kD + dc * 8)
-                                 : make_uint4(0, 0, 0, 0);
+    for (int u = 0; u < LPH; ++u) {
+        const int r = (u * NW + wave) * 8 + (lane >> 3);
+        doff[u] = (unsigned int)(r * 128 + (((lane & 7) ^ swz(r)) << 4));
+    }
+    // Rows row0..row0+63 of one tensor into a half slot; rows past N repeat row N-1.
+    auto dma_half = [&](const unsigned char *src, int row0, unsigned char *dst) __attribute__((always_inline)) {
+        if (row0 + 64 <= N) {
+            const unsigned char *s = src + (size_t)row0 * 128;
+#pragma unroll
+            for (int u = 0; u < LPH; ++u)
+                __builtin_amdgcn_global_load_lds((const void *)(s + doff[u]), (lds_void *)(dst + (u * NW + wave) * 1024), 16, 0, 0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < LPH; ++u) {
+                const int r = (u * NW + wave) * 8 + (lane >> 3);
+                const int row = min(row0 + r, N - 1);
+                __builtin_amdgcn_global_load_lds((const void *)(src + (size_t)row * 128 + (doff[u] & 127)),
+                                                 (lds_void *)(dst + (u * NW + wave) * 1024), 16, 0, 0);
             }
         }
     };
-    auto store_tile = [&]() {
-#pragma unroll
-        for (int u = 0; u < KU; ++u) {
-            const int unit = tid + u * T, kr = unit >> 3, ch = unit & 7;
-            *reinterpret_cast<uint4 *>(k_lds + kr * 128 + (k_chunk(kr, ch) << 4)) = kreg[u];
-        }
-#pragma unroll
-        for (int u = 0; u < VU; ++u) {
-            const int unit = tid + u * T;
-            if (unit >= VUNITS) continue;
-            const int kg = unit >> 3, dc = unit & 7;
-            const int pos = (kg >> 2) * 16 + vt_pos((kg & 3) * 4);  // V^T position of key 4*kg
-            const unsigned int w[4][4] = {{vreg[u][0].x, vreg[u][0].y, vreg[u][0].z, vreg[u][0].w},
-                                          {vreg[u][1].x, vreg[u][1].y, vreg[u][1].z, vreg[u][1].w},
-                                          {vreg[u][2].x, vreg[u][2].y, vreg[u][2].z, vreg[u][2].w},
-                                          {vreg[u][3].x, vreg[u][3].y, vreg[u][3].z, vreg[u][3].w}};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {  // channels 2e, 2e+1 of this unit
-                // v_perm_b32 picks the low (even channel) or high (odd channel) halves of
-                // two keys' words: {key b low half, key a low half} etc.
-                const unsigned int lo01 = __builtin_amdgcn_perm(w[1][e], w[0][e], 0x05040100u);
-                const unsigned int lo23 = __builtin_amdgcn_perm(w[3][e], w[2][e], 0x05040100u);
-                const unsigned int hi01 = __builtin_amdgcn_perm(w[1][e], w[0][e], 0x07060302u);
-                const unsigned int hi23 = __builtin_amdgcn_perm(w[3][e], w[2][e], 0x07060302u);
-                const int d0 = dc * 8 + 2 * e, d1 = d0 + 1;
-                *reinterpret_cast<uint2 *>(v_lds + d0 * VROW + (v_chunk<BK>(d0, pos >> 3) << 4) + (pos & 7) * 2) =
-                    make_uint2(lo01, lo23);
-                *reinterpret_cast<uint2 *>(v_lds + d1 * VROW + (v_chunk<BK>(d1, pos >> 3) << 4) + (pos & 7) * 2) =
-                    make_uint2(hi01, hi23);
-            }
-        }
+    auto dma_tile = [&](const unsigned char *src, const int (&jt)[EPT], unsigned char *dst) __attribute__((always_inline)) {
+        dma_half(src, half_row0(jt, 0), dst);
+        dma_half(src, half_row0(jt, 1), dst + HALF);
     };
+
+    // Per-lane LDS byte offsets of the operand reads (tile-relative; the key
+    // offset of a half / sub-tile is added as an immediate).
+    int koff[4];  // score operand: key ql, logical chunk 2kk+hh
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) koff[kk] = ql * 128 + (((2 * kk + hh) ^ swz(ql)) << 4);
+    int voff[2][2];  // transpose reads: key 8r + 4hh + s16/4, channels 32dh + 16g16 + 4(s16&3)
+#pragma unroll
+    for (int dh = 0; dh < 2; ++dh)
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int key = 8 * r + 4 * hh + (s16 >> 2);
+            const int d = 32 * dh + 16 * g16 + 4 * (s16 & 3);
+            voff[dh][r] = key * 128 + (((d >> 3) ^ swz(key)) << 4) + (d & 7) * 2;
+        }
 
     const float c = p.scale_log2;
-    float mref = -INFINITY;  // running reference maximum of this lane's query row
+    float mref = -INFINITY;  // reference maximum of this lane's query row (shared with lane^32)
     float lrow = 0.f;
     f32x16 acc_o[2];
 #pragma unroll
@@ -174,44 +209,83 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
         for (int v = 0; v < 16; ++v) acc_o[dh][v] = 0.f;
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-    // One key block: scores, online softmax, PV; nvalid < BK masks a partial block.
-    auto process = [&](int nvalid) {
-        f32x16 s[NT];
+    // S^T of one half: two 32-key sub-tiles, 4 MFMAs each.
+    auto qk = [&](const unsigned char *kt, int hf, f32x16 (&s)[2]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
+        for (int t = 0; t < 2; ++t) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) s[t][v] = 0.f;
-            const int kr = t * 32 + ql;
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
-                const int ch = kk * 2 + hh;
-                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(k_lds + kr * 128 + (k_chunk(kr, ch) << 4));
+                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + hf * HALF + t * 32 * 128 + koff[kk]);
                 s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[t], 0, 0, 0);
             }
         }
-        if (nvalid < BK) {
-            // A real branch: only partial blocks pay for the mask (the empty asm
-            // keeps the compiler from if-converting it into every tile).
-            asm volatile("" ::: "memory");
+    };
+    // O^T += V^T P^T for one half, 16 keys per MFMA.
+    auto pv = [&](const unsigned char *vt, int hf, const bf16x8 (&pb)[2][2]) __attribute__((always_inline)) {
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int key = t * 32 + (v >> 2) * 8 + hh * 4 + (v & 3);
-                    if (key >= nvalid) s[t][v] = -INFINITY;
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int dh = 0; dh < 2; ++dh) {
+                    const unsigned char *base = vt + hf * HALF + (t * 32 + u * 16) * 128;
+                    const s16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(base + voff[dh][0]));
+                    const s16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(base + voff[dh][1]));
+                    const bf16x8 a = __builtin_bit_cast(
+                        bf16x8, (short __attribute__((__vector_size__(8 * sizeof(short))))){
+                                    r0[0], r0[1], r0[2], r0[3], r1[0], r1[1], r1[2], r1[3]});
+                    acc_o[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t][u], acc_o[dh], 0, 0, 0);
                 }
+    };
+    auto mask = [&](f32x16 (&s)[2], int nv) __attribute__((always_inline)) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int key = t * 32 + (v >> 2) * 8 + hh * 4 + (v & 3);
+                if (key >= nv) s[t][v] = -INFINITY;
+            }
+    };
+    // Probabilities of sub-tile t (32 keys) of a half against the current
+    // reference; adds the bf16-rounded values to the lane's partial sums.
+    auto probs_part = [&](const f32x16 (&s)[2], bf16x8 (&pb)[2][2], int t, float mc, float &l0,
+                          float &l1) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            float e[8];
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) e[jj] = __builtin_amdgcn_exp2f(fmaf(s[t][u * 8 + jj], c, -mc));
+            pb[t][u] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
+                              (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
+#pragma unroll
+            for (int jj = 0; jj < 8; jj += 4) {
+                l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][u][jj], pb[t][u][jj + 1]}, ones, l0, false);
+                l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][u][jj + 2], pb[t][u][jj + 3]}, ones, l1, false);
+            }
         }
-        float tmax = -INFINITY;
+    };
+    auto ref_mc = [&]() __attribute__((always_inline)) { return mref == -INFINITY ? 0.f : mref * c; };
+    // All probabilities of one half; returns the lane's sum.
+    auto probs = [&](const f32x16 (&s)[2], bf16x8 (&pb)[2][2]) __attribute__((always_inline)) -> float {
+        const float mc = ref_mc();
+        float l0 = 0.f, l1 = 0.f;
+        probs_part(s, pb, 0, mc, l0, l1);
+        probs_part(s, pb, 1, mc, l0, l1);
+        return l0 + l1;
+    };
+    // Accept the half's probabilities, or redo them against the half's true
+    // maximum (rescaling O and the running sum) when they left the safe range.
+    auto settle = [&](const f32x16 (&s)[2], bf16x8 (&pb)[2][2], float lh) __attribute__((always_inline)) {
+        if (__any(!(lh <= kSumLimit) || mref == -INFINITY)) {
+            float tmax = -INFINITY;
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
+            for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) tmax = fmaxf(tmax, s[t][v]);
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-        // Raise the reference maximum only when this tile exceeds it by more than
-        // 2^kRescaleLog2 in probability (or on the first keys of the row).
-        const bool raise = tmax > mref && (mref == -INFINITY || (tmax - mref) * c > kRescaleLog2);
-        if (__any(raise)) {
-            const float mnew = raise ? tmax : mref;
+                for (int v = 0; v < 16; ++v) tmax = fmaxf(tmax, s[t][v]);
+            tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+            const float mnew = fmaxf(mref, tmax);
             const float alpha = mref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((mref - mnew) * c);
             lrow *= alpha;
 #pragma unroll
@@ -219,47 +293,82 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc_o[dh][v] *= alpha;
             mref = mnew;
+            lh = probs(s, pb);
         }
-        const float mc = mref == -INFINITY ? 0.f : mref * c;
-        bf16x8 pb[NT][2];
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                float e[8];
-#pragma unroll
-                for (int jj = 0; jj < 8; ++jj) e[jj] = __builtin_amdgcn_exp2f(fmaf(s[t][u * 8 + jj], c, -mc));
-                pb[t][u] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
-                                  (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
-#pragma unroll
-                for (int jj = 0; jj < 8; jj += 2)
-                    lrow = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][u][jj], pb[t][u][jj + 1]}, ones, lrow,
-                                                           false);
-            }
-        // O^T += V^T P^T, 16 keys per MFMA.
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const int chunk = (2 * t + u) * 2 + hh;
-#pragma unroll
-                for (int dh = 0; dh < 2; ++dh) {
-                    const int dim = dh * 32 + ql;
-                    const bf16x8 a =
-                        *reinterpret_cast<const bf16x8 *>(v_lds + dim * VROW + (v_chunk<BK>(dim, chunk) << 4));
-                    acc_o[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t][u], acc_o[dh], 0, 0, 0);
-                }
-            }
+        lrow += lh;
     };
-    if (ntiles > 0) load_tile(tile_index(0));
-    for (int it = 0; it < ntiles; ++it) {
-        const int j = tile_index(it);
-        const int nvalid = (j >= 0 && j < n_kb) ? min(BK, N - j * BK) : 0;
+    // One pipeline step: softmax of the current half (scores sc, nv real keys)
+    // beside the score MFMAs of the next half (kt, khf -> sn) and the PV MFMAs
+    // of the previous half (probabilities pp, vt, vhf).
+    auto step = [&](f32x16 (&sc)[2], bf16x8 (&pc)[2][2], int nv, f32x16 (&sn)[2], const unsigned char *kt,
+                    int khf, const bf16x8 (&pp)[2][2], const unsigned char *vt, int vhf) __attribute__((always_inline)) {
+        if (nv < 64) {
+            // A real branch: only partial halves pay for the mask (the empty asm
+            // keeps the compiler from if-converting it into every step).
+            asm volatile("" ::: "memory");
+            mask(sc, nv);
+        }
+        // Two scheduling regions. First the score MFMAs of the next half (their
+        // results are consumed at the next step) beside the softmax of sub-tile 0,
+        // then the PV MFMAs of the previous half beside the softmax of sub-tile 1.
+        const float mc = ref_mc();
+        float l0 = 0.f, l1 = 0.f;
+        qk(kt, khf, sn);
+        probs_part(sc, pc, 0, mc, l0, l1);
+        __builtin_amdgcn_sched_barrier(0);
+        pv(vt, vhf, pp);
+        probs_part(sc, pc, 1, mc, l0, l1);
+        const float lh = l0 + l1;
+        settle(sc, pc, lh);
+    };
+
+    f32x16 sA[2], sB[2];
+    bf16x8 pA[2][2], pB[2][2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) pB[t][u] = bf16x8{};
+    int jt0[EPT], jt1[EPT], jt2[EPT];
+
+    // Tile it (it = 0 .. L-1): K in kc, V in vc; K of tile it+1 in kn; V of tile
+    // it-1 in vp. sA holds the scores of (it, half 0), pB the probabilities of
+    // (it-1, half 1).
+    auto iter = [&](int it, unsigned char *kc, const unsigned char *kn, const unsigned char *vc,
+                    unsigned char *vp) __attribute__((always_inline)) {
+        fetch_tile(it + 2, jt2);
+        step(sA, pA, half_keys(jt0, 0), sB, kc, 1, pB, vp, 1);
+        wait_vm_all();    // this wave's loads of K(it+1) and V(it) have landed
+        __syncthreads();  // ... and every wave's; K(it) and V(it-1) are no longer read
+        if (it + 2 < L) dma_tile(kbytes, jt2, kc);
+        if (it + 1 < L) dma_tile(vbytes, jt1, vp);
+        step(sB, pB, half_keys(jt0, 1), sA, kn, 0, pA, vc, 0);
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            jt0[e] = jt1[e];
+            jt1[e] = jt2[e];
+        }
+    };
+
+    if (L > 0) {
+        fetch_tile(0, jt0);
+        fetch_tile(1, jt1);
+        // The first step multiplies zero probabilities with V slot 1, half 1.
+        for (int u = tid; u < HALF / 16; u += T) reinterpret_cast<uint4 *>(v_lds1 + HALF)[u] = make_uint4(0, 0, 0, 0);
+        dma_tile(kbytes, jt0, k_lds0);
+        if (L > 1) dma_tile(kbytes, jt1, k_lds1);
+        dma_tile(vbytes, jt0, v_lds0);
+        wait_vm_all();
         __syncthreads();
-        store_tile();
-        __syncthreads();
-        if (it + 1 < ntiles) load_tile(tile_index(it + 1));
-        process(nvalid);
+        qk(k_lds0, 0, sA);
+        int it = 0;
+        for (;;) {
+            iter(it, k_lds0, k_lds1, v_lds0, v_lds1);
+            if (++it >= L) break;
+            iter(it, k_lds1, k_lds0, v_lds1, v_lds0);
+            if (++it >= L) break;
+        }
+        // PV of the last half; its tile sits in V slot (L-1) % 2.
+        pv((L & 1) ? v_lds0 : v_lds1, 1, pB);
     }
 
     // Each lane summed half of its row's keys; lanes l and l^32 share the row.

@@ -20,7 +20,7 @@ int check_shape(const ress_shape *s, Grid *g)
     if (s->H < 0 || s->N < 0 || s->n_special_tail < 0 || s->n_special_tail > s->N) return RESS_E_INVALID_ARG;
     if (s->D != kD) return RESS_E_UNSUPPORTED;
     if ((s->bq != 64 && s->bq != 128) || (s->bk != 64 && s->bk != 128)) return RESS_E_UNSUPPORTED;
-    if (s->H > RESS_MAX_HEADS) return RESS_E_UNSUPPORTED;
+    if (s->H > RESS_MAX_HEADS || s->N > RESS_MAX_TOKENS) return RESS_E_UNSUPPORTED;
     g->n_qb = ((long long)s->N + s->bq - 1) / s->bq;
     g->n_kb = ((long long)s->N + s->bk - 1) / s->bk;
     return RESS_OK;
@@ -29,6 +29,7 @@ int check_shape(const ress_shape *s, Grid *g)
 bool has_work(const ress_shape *s) { return s->H > 0 && s->N > 0; }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+bool aligned16(const void *ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 
 // Workspace: qbar [H][n_qb][64], then kbarT, vbar, vbarT, uT, each [H][n_kb][64]
 // (float64), every region 256-byte aligned.
@@ -86,6 +87,7 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
         return RESS_E_INVALID_ARG;
     if (!has_work(shape)) return RESS_OK;
     if (!q || !k || !v || !gram || !keep_budget || !kept_count || !kept_idx) return RESS_E_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return RESS_E_INVALID_ARG;
 
     const int n_kb = (int)g.n_kb, n_qb = (int)g.n_qb;
     const int first_forced = first_forced_block(shape, g);
@@ -161,6 +163,7 @@ static int attn_common(const ress_shape *shape, const void *q, const void *k, co
     if (!has_work(shape)) return RESS_OK;
     if (!q || !k || !v || !o) return RESS_E_INVALID_ARG;
     if (o == q || o == k || o == v) return RESS_E_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return RESS_E_INVALID_ARG;
     if (sparse && (!kept_count || !kept_idx)) return RESS_E_INVALID_ARG;
     const long long items = (long long)shape->H * g.n_qb;
     const long long per_xcd = (items + 7) / 8;

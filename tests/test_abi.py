@@ -62,6 +62,7 @@ def test_workspace_size(ress):
     assert _ws(ress, bq=96)[0] == ress.RESS_E_UNSUPPORTED
     assert _ws(ress, H=257)[0] == ress.RESS_E_UNSUPPORTED
     assert _ws(ress, N=-1)[0] == ress.RESS_E_INVALID_ARG
+    assert _ws(ress, N=(1 << 24) + 1, H=1, n_special_tail=0)[0] == ress.RESS_E_UNSUPPORTED
     assert _ws(ress, n_special_tail=43969)[0] == ress.RESS_E_INVALID_ARG
     shape = ress.make_shape(16, 100, bq=64, bk=64, D=32)
     assert ress.lib.ress_select_workspace_size(C.byref(shape), C.byref(C.c_size_t())) == ress.RESS_E_UNSUPPORTED
@@ -96,6 +97,7 @@ def test_select_rejects_before_launch(ress):
     one_forced = ress.make_shape(2, 1230, bq=64, bk=64, n_special_tail=10)  # only block 19 forced
     assert _select_status(ress, one_forced, good, [0, 6]) == ress.RESS_E_INVALID_ARG
     assert _select_status(ress, shape, good, [6, 6], ptr=0) == ress.RESS_E_INVALID_ARG
+    assert _select_status(ress, shape, good, [6, 6], ptr=(1 << 41) + 8) == ress.RESS_E_INVALID_ARG  # q/k/v not 16-byte aligned
     empty = ress.make_shape(0, 1230, bq=64, bk=64)
     assert _select_status(ress, empty, good, [], ptr=0, ws_ptr=0, ws_bytes=0) == ress.RESS_OK
 
@@ -112,6 +114,12 @@ def test_attention_rejects_before_launch(ress):
                                     None) == ress.RESS_E_INVALID_ARG  # o aliases q
     assert ress.lib.ress_sparse_attn(C.byref(shape), p, C.c_void_p(1 << 43), C.c_void_p(1 << 44), None, p,
                                      0.125, o, None) == ress.RESS_E_INVALID_ARG
+    for misaligned in ((p, C.c_void_p((1 << 43) + 2), C.c_void_p(1 << 44), o),
+                       (p, C.c_void_p(1 << 43), C.c_void_p(1 << 44), C.c_void_p((1 << 42) + 8))):
+        assert ress.lib.ress_dense_attn(C.byref(shape), misaligned[0], misaligned[1], misaligned[2], 0.125,
+                                        misaligned[3], None) == ress.RESS_E_INVALID_ARG
+    huge = ress.make_shape(1, (1 << 24) + 1, bq=128, bk=128)
+    assert ress.lib.ress_dense_attn(C.byref(huge), p, p, p, 0.125, o, None) == ress.RESS_E_UNSUPPORTED
     bad = ress.make_shape(2, 1230, bq=32, bk=64)
     assert ress.lib.ress_dense_attn(C.byref(bad), p, p, p, 0.125, o, None) == ress.RESS_E_UNSUPPORTED
     empty = ress.make_shape(2, 0, bq=64, bk=64)
