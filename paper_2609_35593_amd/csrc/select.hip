@@ -515,8 +515,8 @@ hipError_t launch_select(const SelectParams &p, hipStream_t s)
     if (n <= 128) return launch_cfg<2, 4>(p, s);
     if (n <= 256) return launch_cfg<4, 4>(p, s);
     if (n <= 384) return launch_cfg<6, 2>(p, s);
-    if (n <= 512) return launch_cfg<8, 2>(p, s);
-    if (n <= 768) return launch_cfg<12, 2>(p, s);
+    if (n <= 512) return launch_cfg<8, 1>(p, s);
+    if (n <= 768) return launch_cfg<12, 1>(p, s);
     if (n <= 1088) return launch_cfg<17, 1>(p, s);
     if (n <= 1536) return launch_cfg<24, 1>(p, s);
     if (n <= 2048) return launch_cfg<32, 1>(p, s);

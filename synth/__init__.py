@@ -183,7 +183,9 @@ def stack_sigma(layer: int, n_layers: int = 24) -> float:
     return 0.3 + 0.7 * layer / (n_layers - 1)
 
 
-def make_config(name: str, sparsity=None, layer: int = 0, H: int = 16) -> Layer:
+def make_config(name: str, sparsity=None, layer: int = 0, H: int = 16, bq=None, bk=None) -> Layer:
+    """One layer of a named workload; bq / bk override its block sizes (for
+    instance the 128-query / 64-key grid)."""
     cfg = CONFIGS[name]
     seed = 1000 + cfg["index"] + (layer if name == "16v_stack" else 0)
     sigma = stack_sigma(layer) if name == "16v_stack" else 0.5
@@ -192,4 +194,4 @@ def make_config(name: str, sparsity=None, layer: int = 0, H: int = 16) -> Layer:
     if isinstance(sparsity, str) and sparsity == "ragged":
         sparsity = np.random.default_rng(seed + 1).uniform(0.80, 0.95, size=H)
     return make_layer(cfg["views"], cfg["patch"], cfg["special"], H=H, block=cfg["block"],
-                      sigma=sigma, sparsity=sparsity, seed=seed, name=name)
+                      sigma=sigma, sparsity=sparsity, seed=seed, name=name, bq=bq, bk=bk)

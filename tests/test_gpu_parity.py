@@ -142,6 +142,28 @@ def test_config_32v(ress, sparsity, rounds):
     _config_case(ress, synth.make_config("32v", sparsity=sparsity), rounds, label=f"32v s={sparsity} R={rounds}")
 
 
+def test_config_32v_q128_k64(ress):
+    """The paper's own grid: 128-token query blocks, 64-token key blocks (687 key
+    blocks per head at 32 views, so 12 slots per lane in the selection and two
+    kept blocks per 128-key attention tile). Oracle on a row sample."""
+    L = synth.make_config("32v", sparsity=0.75, bk=64)
+    assert (L.bq, L.bk, L.n_kb) == (128, 64, 687)
+    rng = np.random.default_rng(11)
+    rows = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 600),
+                                     [h * L.n_qb + i for h in range(L.H) for i in (0, L.n_qb - 1, L.n_qb - 2)]]))
+    _config_case(ress, L, 5, rows=rows, n_tokens=384, label="32v q128/k64")
+
+
+def test_select_one_row_per_wave_range(ress):
+    """385-768 key blocks run one row per wave (8 slots per lane here): 22 views on
+    the 128/64 grid, 473 key blocks, oracle on a row sample."""
+    L = synth.make_layer(22, 1369, 5, H=4, bq=128, bk=64, sparsity=0.8, seed=33, name="22v q128/k64")
+    assert 384 < L.n_kb <= 512
+    rng = np.random.default_rng(12)
+    rows = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 300), [L.n_qb - 1, 0]]))
+    _config_case(ress, L, 5, rows=rows, n_tokens=256, label="22v q128/k64")
+
+
 def test_config_100v_ragged(ress):
     L = synth.make_config("100v")
     rng = np.random.default_rng(5)
