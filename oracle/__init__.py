@@ -57,10 +57,10 @@ def lib(path: str | None = None):
         L.ro_deltas.argtypes = [i, i, _dp, _dp, _dp, _dp, _dp, _u8, _u8, d, _dp]
         L.ro_swaps.argtypes = [i, d, i, i]
         L.ro_swaps.restype = i
-        L.ro_select_row.argtypes = [i, i, _dp, _dp, _dp, _dp, _u8, i, i, d, d, i, i, _u8, _dp, _dp,
+        L.ro_select_row.argtypes = [i, i, _dp, _dp, _dp, _dp, _u8, i, i, d, d, i, i, i, d, _u8, _dp, _dp,
                                     C.POINTER(d), C.POINTER(d), C.POINTER(d), _opt(_dp), _opt(_u8),
                                     C.POINTER(i)]
-        L.ro_select.argtypes = [i, i, i, i, i, i, _u16, _u16, _u16, _fp, _i32, i, d, d, i, i, i,
+        L.ro_select.argtypes = [i, i, i, i, i, i, _u16, _u16, _u16, _fp, _i32, i, d, d, i, i, i, d, i,
                                 _opt(_i32), _i32, _i32, _opt(_dp), _opt(_dp), _opt(_dp), _opt(_dp)]
         L.ro_select.restype = i
         L.ro_attn_tokens.argtypes = [i, i, i, i, i, _u16, _u16, _u16, d, _opt(_i32), _opt(_i32), i,
@@ -168,8 +168,13 @@ def swaps(c: int, rho: float, r: int, swap_floor: int = 1) -> int:
     return _L().ro_swaps(int(c), float(rho), int(r), int(swap_floor))
 
 
+# Selection criteria (the paper's comparisons, Secs. 5.3-5.4, Table 3; see the list
+# at the top of ress_oracle.c).
+DRIFT, PROBABILITY, DRIFT_MAX_SWAP, DRIFT_MAX_FULL = 0, 1, 2, 3
+
+
 def select_row(qbar_i, kbar, vbar, M, forced, c, rounds=5, rho=0.5, eps=1e-4, swap_floor=1,
-               dense_row=False):
+               dense_row=False, criterion=DRIFT, cdf_tau=0.0):
     """Secs. 4.2-4.3 for one row, with the trajectory of drop sets."""
     kbar, vbar = _c(kbar, np.float64), _c(vbar, np.float64)
     nkb, D = kbar.shape
@@ -182,7 +187,8 @@ def select_row(qbar_i, kbar, vbar, M, forced, c, rounds=5, rho=0.5, eps=1e-4, sw
     ns = C.c_int()
     _L().ro_select_row(D, nkb, _c(qbar_i, np.float64), kbar, vbar, _c(M, np.float64),
                         _c(forced, np.uint8), int(c), int(rounds), float(rho), float(eps),
-                        int(swap_floor), int(bool(dense_row)), kept, P, key, C.byref(J0),
+                        int(swap_floor), int(bool(dense_row)), int(criterion), float(cdf_tau), kept, P, key,
+                        C.byref(J0),
                         C.byref(Jb), C.byref(mg), tJ, tD, C.byref(ns))
     n = ns.value
     return dict(kept=kept.astype(bool), P=P, key=key, J_init=J0.value, J_best=Jb.value,
@@ -190,7 +196,8 @@ def select_row(qbar_i, kbar, vbar, M, forced, c, rounds=5, rho=0.5, eps=1e-4, sw
 
 
 def select(q, k, v, gram, budgets, *, N, bq, bk, n_special, rounds=5, rho=0.5, eps=1e-4,
-           swap_floor=1, dense_special_queries=True, rows=None, want_key=True):
+           swap_floor=1, dense_special_queries=True, rows=None, want_key=True, criterion=DRIFT,
+           cdf_tau=0.0):
     """Selection for every row (rows=None) or for the flat rows h * n_qb + i given.
     Returns kept_count [R], kept_idx [R][n_kb], drift [R][2], key/prob [R][n_kb], margin [R]."""
     q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
@@ -206,7 +213,8 @@ def select(q, k, v, gram, budgets, *, N, bq, bk, n_special, rounds=5, rho=0.5, e
     margin = np.zeros(R)
     _L().ro_select(H, N, D, bq, bk, n_special, q, k, v, _c(gram, np.float32),
                     _c(budgets, np.int32), int(rounds), float(rho), float(eps), int(swap_floor),
-                    int(bool(dense_special_queries)), R, rws, kc, ki, drift, key, prob, margin)
+                    int(bool(dense_special_queries)), int(criterion), float(cdf_tau), R, rws, kc, ki, drift,
+                    key, prob, margin)
     return dict(kept_count=kc, kept_idx=ki, drift=drift, key=key, prob=prob, margin=margin)
 
 

@@ -33,6 +33,16 @@
  *   - swaps are always applied; track-best keeps the first drop set with the
  *     strictly smallest J, counting the initial one;
  *   - query blocks that hold special tokens attend densely when asked to.
+ *
+ * Selection criteria (the paper's comparisons, Secs. 5.3-5.4 and Table 3):
+ *   0  drift (ReSS): keep the c largest keys, rounds minimise J;
+ *   1  probability (the SparseVGGT rule): keep the c largest P; optionally capped
+ *      by a CDF threshold tau: the shortest prefix in descending P whose mass,
+ *      counting the always-kept forced blocks, reaches tau (never below the
+ *      two-block floor); rounds, if any, minimise J for the realised count;
+ *   2  drift maximisation in the rounds only: initial set as in 0, rounds pick the
+ *      swaps that raise J most, track-best keeps the largest J;
+ *   3  drift maximisation throughout: keep the c smallest keys, rounds as in 2.
  */
 #include <math.h>
 #include <stdint.h>
@@ -273,6 +283,7 @@ static double min2(double a, double b) { return a < b ? a : b; }
  *   forced[j]  key block j is always kept (not a candidate)
  *   c          keep budget c_h (number of kept candidates)
  *   dense_row  the row keeps every block (special-token query block)
+ *   criterion, cdf_tau  see the list of criteria at the top of this file
  * Outputs: kept[j] (1 = kept), P, key (forced blocks get key -1), J_init, J_best,
  * margin (smallest relative decision gap along the trajectory), and optionally
  * the trajectory: trace_J[s] and trace_D[s][j] for stages s = 0 (initial set) ..
@@ -280,6 +291,7 @@ static double min2(double a, double b) { return a < b ? a : b; }
 void ro_select_row(int D, int nkb, const double *qbar_i, const double *kbar,
                    const double *vbar, const double *M, const unsigned char *forced, int c,
                    int rounds, double rho, double eps, int swap_floor, int dense_row,
+                   int criterion, double cdf_tau,
                    unsigned char *kept, double *P, double *key, double *J_init,
                    double *J_best, double *margin, double *trace_J,
                    unsigned char *trace_D, int *n_stages)
@@ -315,13 +327,49 @@ void ro_select_row(int D, int nkb, const double *qbar_i, const double *kbar,
         goto done;
     }
 
-    /* Initial selection (Eq. 7): keep the c largest keys among the candidates. */
+    /* Initial selection (Eq. 7): keep the c largest keys among the candidates
+     * (criterion 1: the c largest P; criterion 3: the c smallest keys). */
+    const int maximise = criterion == 2 || criterion == 3;
     {
-        double gap = top_k(nkb, key, cand, c, sel);
-        double kmax = 0.0;
+        double *rank = dJ; /* scratch: the ranking value of each block */
+        for (int j = 0; j < nkb; ++j) rank[j] = criterion == 1 ? P[j] : criterion == 3 ? -key[j] : key[j];
+        if (criterion == 1 && cdf_tau > 0.0) {
+            /* CDF cap: shortest prefix (P descending, lower index first) whose mass
+             * together with the forced blocks reaches tau. */
+            int n_forced = 0;
+            double mass = 0.0;
+            for (int j = 0; j < nkb; ++j)
+                if (forced[j]) {
+                    ++n_forced;
+                    mass += P[j];
+                }
+            int lo = 2 - n_forced > 0 ? 2 - n_forced : 0;
+            if (lo > n_p) lo = n_p;
+            ro_item *it = (ro_item *)malloc(sizeof(ro_item) * (n_p > 0 ? n_p : 1));
+            int cnt = 0;
+            for (int j = 0; j < nkb; ++j)
+                if (cand[j]) {
+                    it[cnt].v = P[j];
+                    it[cnt].j = j;
+                    ++cnt;
+                }
+            qsort(it, (size_t)cnt, sizeof(ro_item), item_cmp);
+            int n = 0;
+            while (n < cnt && mass < cdf_tau) mass += it[n++].v;
+            /* decision margin of the cut: distance of the two partial sums around it */
+            if (n > 0 && n <= cnt && n < c) {
+                double before = mass - it[n - 1].v;
+                mrg = min2(mrg, min2(mass - cdf_tau, cdf_tau - before) / cdf_tau);
+            }
+            free(it);
+            if (n < lo) n = lo;
+            if (n < c) c = n;
+        }
+        double gap = top_k(nkb, rank, cand, c, sel);
+        double vmax = 0.0;
         for (int j = 0; j < nkb; ++j)
-            if (cand[j] && key[j] > kmax) kmax = key[j];
-        if (c > 0) mrg = min2(mrg, gap / (kmax > 0.0 ? kmax : 1e-300));
+            if (cand[j] && fabs(rank[j]) > vmax) vmax = fabs(rank[j]);
+        if (c > 0) mrg = min2(mrg, gap / (vmax > 0.0 ? vmax : 1e-300));
     }
     for (int j = 0; j < nkb; ++j) inD[j] = cand[j] && !sel[j];
     double J = ro_objective(D, nkb, P, vbar_i, vbar, M, inD, eps, NULL, NULL, NULL);
@@ -342,6 +390,8 @@ void ro_select_row(int D, int nkb, const double *qbar_i, const double *kbar,
         if (m > nS) m = nS;
         if (m <= 0) break;
         ro_deltas(D, nkb, P, s, vbar_i, vbar, M, inD, cand, eps, dJ);
+        if (maximise) /* the best swaps now raise J the most */
+            for (int j = 0; j < nkb; ++j) dJ[j] = -dJ[j];
         unsigned char *memD = sel, *memS = pick; /* reuse buffers */
         unsigned char *restore = (unsigned char *)malloc(nkb);
         unsigned char *drop = (unsigned char *)malloc(nkb);
@@ -364,7 +414,7 @@ void ro_select_row(int D, int nkb, const double *qbar_i, const double *kbar,
         /* The track-best comparison decides the output only when this stage's
          * drop set differs from the best one (a set revisited has the same J). */
         if (memcmp(inD, best, nkb) != 0) mrg = min2(mrg, fabs(J - Jb) / (Jb > 0.0 ? Jb : 1e-300));
-        if (J < Jb) {
+        if (maximise ? J > Jb : J < Jb) {
             Jb = J;
             memcpy(best, inD, nkb);
         }
@@ -406,6 +456,7 @@ static int special_query_block(int N, int bq, int n_special, int i)
 int ro_select(int H, int N, int D, int bq, int bk, int n_special, const uint16_t *q,
               const uint16_t *k, const uint16_t *v, const float *gram, const int *budgets,
               int rounds, double rho, double eps, int swap_floor, int dense_special_queries,
+              int criterion, double cdf_tau,
               int n_rows, const int *rows, int *kept_count, int *kept_idx, double *drift,
               double *key, double *prob, double *margin)
 {
@@ -433,8 +484,8 @@ int ro_select(int H, int N, int D, int bq, int bk, int n_special, const uint16_t
         int dense = dense_special_queries && special_query_block(N, bq, n_special, i);
         ro_select_row(D, nkb, qbar + ((size_t)h * nqb + i) * D, kbar + (size_t)h * nkb * D,
                       vbar + (size_t)h * nkb * D, M + (size_t)h * D * D, forced, budgets[h],
-                      rounds, rho, eps, swap_floor, dense, kept, P, ky, &J0, &Jb, &mg, NULL,
-                      NULL, NULL);
+                      rounds, rho, eps, swap_floor, dense, criterion, cdf_tau, kept, P, ky, &J0,
+                      &Jb, &mg, NULL, NULL, NULL);
         int cnt = 0;
         for (int j = 0; j < nkb; ++j)
             if (kept[j]) kept_idx[(size_t)r * nkb + cnt++] = j;

@@ -86,6 +86,17 @@ def brute_force_min(logits, vbar, M, cand: np.ndarray, c: int):
     return best, best_set
 
 
+def brute_force_max(logits, vbar, M, cand: np.ndarray, c: int):
+    """Largest drift over every drop set of size |P| - c (the sign-flipped problem)."""
+    idx = np.flatnonzero(cand)
+    best = -math.inf
+    for keep in itertools.combinations(idx.tolist(), c):
+        drop = cand.copy()
+        drop[list(keep)] = False
+        best = max(best, drift_sq_m(logits, vbar, M, drop))
+    return best
+
+
 def row_inputs(layer, h: int, i: int, pooled=None):
     """Pooled inputs of row (h, i): qbar_i, kbar, vbar (float64), M (float64 of the
     float32 Gram), forced mask, budget, W_O slice."""

@@ -301,6 +301,115 @@ def check_brute_force(report=None):
                     report.append(res["J_best"] / jstar if jstar > 0 else 1.0)
 
 
+# --------------------------------------------------------------------------- other criteria
+# (the paper's comparisons: probability selection and its CDF threshold, Table 3;
+# drift maximisation, Sec. 5.4)
+
+
+def check_probability_criterion():
+    """Probability criterion: the kept candidates are the c largest pooled
+    probabilities (softmax of the pooled logits, computed here), ties to the lower
+    index; with rounds the stages still have exact drifts and track-best minimises."""
+    for name in ("forced", "plain", "ragged"):
+        for h, i in rows_of(name, 2):
+            r = _row(name, h, i)
+            cand, c = ~r["forced"], r["c"]
+            P = softmax(r["logits"])
+            res = oracle.select_row(r["qbar_i"], r["kbar"], r["vbar"], r["M"], r["forced"], c, rounds=0,
+                                    criterion=oracle.PROBABILITY)
+            ref, gap = direct.top_by(P, cand, c)
+            if gap > 1e-12:
+                assert np.array_equal(res["kept"], r["forced"] | ref), (name, h, i)
+            res5 = oracle.select_row(r["qbar_i"], r["kbar"], r["vbar"], r["M"], r["forced"], c, rounds=5,
+                                     criterion=oracle.PROBABILITY)
+            for st in range(len(res5["trace_D"])):
+                np.testing.assert_allclose(res5["trace_J"][st],
+                                           direct.drift_sq_m(r["logits"], r["vbar"], r["M"], res5["trace_D"][st]),
+                                           rtol=1e-9, atol=1e-300)
+            assert res5["J_best"] == res5["trace_J"].min() and res5["J_best"] <= res5["J_init"]
+            assert res5["kept"].sum() == c + r["forced"].sum()
+
+
+def check_cdf_threshold():
+    """CDF cap on the probability criterion: the kept candidates are a prefix of the
+    candidates in descending probability; unless the budget or the two-block floor
+    binds, the kept mass (forced blocks included) reaches tau and dropping the last
+    kept candidate would fall below it."""
+    for name in ("forced", "plain"):
+        for h, i in rows_of(name, 2):
+            r = _row(name, h, i)
+            cand, c = ~r["forced"], r["c"]
+            P = softmax(r["logits"])
+            floor = max(0, 2 - int(r["forced"].sum()))
+            for tau in (0.2, 0.5, 0.8, 0.95):
+                res = oracle.select_row(r["qbar_i"], r["kbar"], r["vbar"], r["M"], r["forced"], c, rounds=0,
+                                        criterion=oracle.PROBABILITY, cdf_tau=tau)
+                kept_c = res["kept"] & cand
+                n = int(kept_c.sum())
+                assert floor <= n <= c, (name, h, i, tau, n)
+                ref, gap = direct.top_by(P, cand, n)
+                if gap > 1e-12:
+                    assert np.array_equal(kept_c, ref), (name, h, i, tau)
+                mass = P[r["forced"]].sum() + P[kept_c].sum()
+                smallest = P[kept_c].min() if n else 0.0
+                if abs(mass - tau) > 1e-12 and abs(mass - smallest - tau) > 1e-12:
+                    if floor < n < c:
+                        assert mass >= tau and mass - smallest < tau, (name, h, i, tau, n, mass)
+                    elif n == c:  # the budget binds: the prefix one shorter never reached tau
+                        assert c == 0 or mass - smallest < tau, (name, h, i, tau, n, mass)
+
+
+def check_drift_max():
+    """Sign-flipped objective (Sec. 5.4). Full flip with no rounds keeps the c
+    smallest single-block drifts J({j}) = key_j^2; in the rounds every swap is the
+    one that raises J most (at the round-start set), track-best keeps the largest J,
+    and on small rows the result never exceeds the brute-force maximum."""
+    for name in ("forced", "plain"):
+        for h, i in rows_of(name, 2):
+            r = _row(name, h, i)
+            cand, c = ~r["forced"], r["c"]
+            Jm = lambda d: direct.drift_sq_m(r["logits"], r["vbar"], r["M"], d)
+            single = np.array([Jm(np.eye(len(cand), dtype=bool)[j]) if cand[j] else 0.0 for j in range(len(cand))])
+            res0 = oracle.select_row(r["qbar_i"], r["kbar"], r["vbar"], r["M"], r["forced"], c, rounds=0,
+                                     criterion=oracle.DRIFT_MAX_FULL)
+            ref, gap = direct.top_by(-single, cand, c)
+            if gap > 1e-9 * max(single.max(), 1e-300):
+                assert np.array_equal(res0["kept"], r["forced"] | ref), (name, h, i)
+            for crit in (oracle.DRIFT_MAX_SWAP, oracle.DRIFT_MAX_FULL):
+                res = oracle.select_row(r["qbar_i"], r["kbar"], r["vbar"], r["M"], r["forced"], c, rounds=5,
+                                        criterion=crit)
+                tD, tJ = res["trace_D"], res["trace_J"]
+                best = int(np.argmax(tJ))  # first maximum
+                assert res["J_best"] == tJ[best] and res["J_best"] >= res["J_init"]
+                assert np.array_equal(res["kept"], r["forced"] | (cand & ~tD[best]))
+                n_p = cand.sum()
+                for st in range(len(tD) - 1):
+                    Ds, Dn = tD[st], tD[st + 1]
+                    A, B = Ds & ~Dn, Dn & ~Ds
+                    m = min(_schedule(c, st), n_p - c, c)
+                    assert A.sum() == m and B.sum() == m
+                    Js = Jm(Ds)
+                    rise = np.full(len(cand), -np.inf)
+                    for k in np.flatnonzero(cand):
+                        nd = Ds.copy()
+                        nd[k] = not nd[k]
+                        rise[k] = Jm(nd) - Js
+                    for chosen, member in ((A, Ds), (B, cand & ~Ds)):
+                        want, g2 = direct.top_by(rise, member, m)
+                        if g2 > 1e-9 * Js:
+                            assert np.array_equal(chosen, want), (name, h, i, st, crit)
+    L = layer("brute")
+    for h in range(L.H):
+        for i in range(0, L.n_qb, 3):
+            r = _row("brute", h, i)
+            cand = ~r["forced"]
+            for c in (3, 8):
+                res = oracle.select_row(r["qbar_i"], r["kbar"], r["vbar"], r["M"], r["forced"], c, rounds=5,
+                                        criterion=oracle.DRIFT_MAX_FULL)
+                jmax = direct.brute_force_max(r["logits"], r["vbar"], r["M"], cand, c)
+                assert res["J_best"] <= jmax * (1 + 1e-9)
+
+
 # --------------------------------------------------------------------------- driver
 
 
@@ -409,4 +518,5 @@ def check_zero_sparsity():
 ALL = [check_pool, check_forced, check_pooled_map, check_single_mask, check_scores,
        check_key_singleton, check_two_block, check_objective, check_deltas, check_schedule,
        check_trajectory, check_track_best, check_ties, check_brute_force, check_select_driver,
-       check_edges, check_attention, check_zero_sparsity]
+       check_edges, check_attention, check_zero_sparsity, check_probability_criterion,
+       check_cdf_threshold, check_drift_max]

@@ -18,7 +18,13 @@ MUTATIONS = {
     "tie_to_higher_index": ("return (a->j < b->j) ? -1 : (a->j > b->j);",
                             "return (a->j > b->j) ? -1 : (a->j < b->j);"),
     "schedule_off_by_one": ("ldexp(1.0, -(r + 1))", "ldexp(1.0, -r)"),
-    "no_track_best": ("if (J < Jb) {", "if (1) {"),
+    "no_track_best": ("if (maximise ? J > Jb : J < Jb) {", "if (1) {"),
+    "max_keeps_smallest_J": ("if (maximise ? J > Jb : J < Jb) {", "if (J < Jb) {"),
+    "max_without_gain_flip": ("            for (int j = 0; j < nkb; ++j) dJ[j] = -dJ[j];\n", "            ;\n"),
+    "probability_ranks_by_key": ("rank[j] = criterion == 1 ? P[j] :", "rank[j] = criterion == 1 ? key[j] :"),
+    "cdf_one_block_too_many": ("            while (n < cnt && mass < cdf_tau) mass += it[n++].v;\n",
+                               "            while (n < cnt && mass < cdf_tau) mass += it[n++].v;\n            if (n < cnt) ++n;\n"),
+    "cdf_ignores_forced_mass": ("                    mass += P[j];\n", ""),
     "drift_without_prob": ("g[d] += P[j] * (vbar_i[d] - vbar[(size_t)j * D + d]);",
                            "g[d] += (vbar_i[d] - vbar[(size_t)j * D + d]);"),
     "pooled_logit_unscaled": ("    double scale = 1.0 / sqrt((double)D);\n    for (int j = 0; j < nkb; ++j) {",
