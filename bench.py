@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--bq", type=int, default=None, help="query block size (default: the workload's)")
     ap.add_argument("--bk", type=int, default=None, help="key block size (default: the workload's)")
     ap.add_argument("--no-flush", action="store_true", help="skip the cache-flushed secondary timing")
+    ap.add_argument("--no-criteria", action="store_true", help="skip the per-criterion drift report")
     ap.add_argument("--rounds", type=int, default=5)
     ap.add_argument("--dense-steps", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
@@ -152,6 +153,37 @@ def measured_ceilings(torch, dev):
     return {"bf16_gemm_8192_tflops": round(gemm_tflops, 1), "copy_1gib_read_plus_write_gbs": round(copy_gbs, 1)}
 
 
+def criteria_report(ress, L, q, k, v, gram, o_dense, stream):
+    """The paper's comparison of selection criteria at one budget (Table 3 rows and
+    the sign-flipped objective of Sec. 5.4), on this synthetic layer: for each
+    criterion the median pooled drift J of the returned selection (over rows that
+    drop blocks) and the token-level residual drift it leaves,
+    sum ||W_O (O_sparse - O_dense)||^2 / sum ||W_O O_dense||^2 over every token and
+    head, with ||W_O x||^2 = x^T M x. Everything runs in this library's kernels;
+    the residual drift is reduced with torch."""
+    import torch
+
+    cases = [("drift, R=5 (ReSS)", 0, 0.0, 5), ("drift, R=0", 0, 0.0, 0), ("probability top-k", 1, 0.0, 0),
+             ("probability top-k + CDF 0.9", 1, 0.9, 0), ("drift maximised, swaps only", 2, 0.0, 5),
+             ("drift maximised, full", 3, 0.0, 5)]
+    gram32 = gram.float()
+    od = o_dense.float()
+    base = torch.einsum("htd,hde,hte->", od, gram32, od).item()
+    rep = []
+    for label, crit, tau, rounds in cases:
+        sel = ress.ress_select(q, k, v, gram, L.budgets, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                               rounds=rounds, criterion=crit, cdf_tau=tau, stream=stream)
+        o = ress.ress_sparse_attn(q, k, v, sel["kept_count"], sel["kept_idx"], bq=L.bq, bk=L.bk, stream=stream)
+        d = o.float() - od
+        resid = torch.einsum("htd,hde,hte->", d, gram32, d).item()
+        dr = sel["drift"].reshape(-1, 2)
+        live = dr[:, 0] > 0
+        kept = sel["kept_count"].sum().item()
+        rep.append({"criterion": label, "J_median": float(dr[live, 1].median().item()) if live.any() else 0.0,
+                    "residual_drift_rel": resid / base, "kept_tiles": int(kept)})
+    return rep
+
+
 def copy_calibration():
     import torch
 
@@ -257,6 +289,7 @@ def main():
     t_dense = float(np.mean([a.elapsed_time(b) for a, b in dev_evs]))
 
     ceilings = measured_ceilings(torch, dev)
+    criteria = None if args.no_criteria else criteria_report(ress, L, q, k, v, gram, od, stream)
 
     kc_h, ki_h, dr = kc.cpu().numpy(), ki.cpu().numpy(), drift.cpu().numpy().reshape(-1, 2)
     flops_kept, kept_tiles = kept_flops(L, kc_h, ki_h)
@@ -325,6 +358,7 @@ def main():
                                                   ceilings["copy_1gib_read_plus_write_gbs"], 4),
             "measured_ceilings": ceilings,
             "cache_flushed": flushed,
+            "criteria_same_budget": criteria,
             "input_generation_s": round(gen_s, 1),
         },
     }

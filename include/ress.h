@@ -58,14 +58,36 @@ typedef struct {
     int n_special_tail; /* trailing special tokens, 0..N */
 } ress_shape;
 
+/* Selection criteria. RESS_CRITERION_DRIFT is the method (Secs. 4.2-4.3); the
+ * others are the comparisons the paper makes with the same budget:
+ *   PROBABILITY     keep the c_h largest pooled probabilities P_ij (the
+ *                   probability rule of the ablation, Table 3); with cdf_tau > 0
+ *                   keep only the shortest prefix in descending P whose mass,
+ *                   the always-kept forced blocks included, reaches cdf_tau (the
+ *                   CDF threshold row of Table 3), never below the two-block
+ *                   floor; the realised count replaces c_h in that row's rounds;
+ *   DRIFT_MAX_SWAP  sign-flipped objective in the rounds only (Sec. 5.4): the
+ *                   initial set as for DRIFT, every round makes the swaps that
+ *                   raise J most, and the largest J seen is kept;
+ *   DRIFT_MAX_FULL  sign flipped from the start: keep the c_h smallest keys, then
+ *                   rounds as for DRIFT_MAX_SWAP.
+ * Restoration (rounds > 0) applies to every criterion. */
+#define RESS_CRITERION_DRIFT 0
+#define RESS_CRITERION_PROBABILITY 1
+#define RESS_CRITERION_DRIFT_MAX_SWAP 2
+#define RESS_CRITERION_DRIFT_MAX_FULL 3
+
 /* Selection parameters (Secs. 4.2-4.3). The paper's values: rounds = 5,
- * rho = 0.5, eps = 1e-4 (Eqs. 7 and 17). */
+ * rho = 0.5, eps = 1e-4 (Eqs. 7 and 17), criterion = RESS_CRITERION_DRIFT,
+ * cdf_tau = 0. */
 typedef struct {
     int rounds;                /* restoration rounds R, 0..RESS_MAX_ROUNDS */
     double rho;                /* total swap budget as a fraction of c_h (Eq. 17), >= 0 */
     double eps;                /* guard of Eq. 7, also applied to K in J and dJ, > 0 */
     int swap_floor;            /* round r swaps max(swap_floor, floor(rho c_h 2^-(r+1))), >= 0 */
     int dense_special_queries; /* nonzero: query blocks holding special tokens keep every key block */
+    int criterion;             /* RESS_CRITERION_*, 0..3 */
+    double cdf_tau;            /* CDF threshold in [0, 1]; 0 = off; nonzero only with PROBABILITY */
 } ress_select_params;
 
 /* Bytes of device workspace ress_select needs for `shape` (pooled tensors,
@@ -94,12 +116,12 @@ int ress_select_workspace_size(const ress_shape *shape, size_t *bytes);
  *                 [min(n_p, max(0, 2 - n_forced)), n_p], n_p = candidates (the
  *                 paper's floor of two kept key blocks per query row, Supp. F)
  *   kept_count    device int32 [H][n_qb] out: kept key blocks per row
- *                 (c_h + n_forced, or n_kb for dense rows)
+ *                 (c_h + n_forced, or n_kb for dense rows; fewer under a CDF cap)
  *   kept_idx      device int32 [H][n_qb][n_kb] out: kept key block indices in
  *                 ascending order, padded with -1
  *   drift         device float64 [H][n_qb][2] out (or NULL): (J of the initial
  *                 selection, J of the returned selection); 0 for rows that drop
- *                 nothing
+ *                 nothing. The criterion changes which selections these are.
  *   key_out       device float64 [H][n_qb][n_kb] out (or NULL): ranking keys of
  *                 Eq. 7; -1 for forced blocks
  *   prob_out      device float64 [H][n_qb][n_kb] out (or NULL): pooled map P

@@ -33,7 +33,11 @@ class ress_shape(C.Structure):
 
 class ress_select_params(C.Structure):
     _fields_ = [("rounds", C.c_int), ("rho", C.c_double), ("eps", C.c_double), ("swap_floor", C.c_int),
-                ("dense_special_queries", C.c_int)]
+                ("dense_special_queries", C.c_int), ("criterion", C.c_int), ("cdf_tau", C.c_double)]
+
+
+# Selection criteria (include/ress.h).
+CRITERION_DRIFT, CRITERION_PROBABILITY, CRITERION_DRIFT_MAX_SWAP, CRITERION_DRIFT_MAX_FULL = 0, 1, 2, 3
 
 
 class RessError(RuntimeError):
@@ -106,9 +110,9 @@ def ress_select_workspace_size(shape: ress_shape) -> int:
 
 def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail: int = 0,
                 rounds: int = 5, rho: float = 0.5, eps: float = 1e-4, swap_floor: int = 1,
-                dense_special_queries: bool = True, kept_count=None, kept_idx=None, drift=None,
-                key_out=None, prob_out=None, want_drift: bool = True, want_debug: bool = False,
-                workspace=None, stream=None) -> dict:
+                dense_special_queries: bool = True, criterion: int = CRITERION_DRIFT, cdf_tau: float = 0.0,
+                kept_count=None, kept_idx=None, drift=None, key_out=None, prob_out=None,
+                want_drift: bool = True, want_debug: bool = False, workspace=None, stream=None) -> dict:
     """Drift-based block selection for one layer (see include/ress.h).
     keep_budget: host int32 [H]. Returns the output tensors in a dict."""
     _check_qkv(q, k, v)
@@ -135,7 +139,8 @@ def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail:
     need = ress_select_workspace_size(shape)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    params = ress_select_params(int(rounds), float(rho), float(eps), int(swap_floor), int(bool(dense_special_queries)))
+    params = ress_select_params(int(rounds), float(rho), float(eps), int(swap_floor), int(bool(dense_special_queries)),
+                                int(criterion), float(cdf_tau))
     st = lib.ress_select(C.byref(shape), C.byref(params), _ptr(q), _ptr(k), _ptr(v), _ptr(gram),
                          budget.ctypes.data, _ptr(kept_count), _ptr(kept_idx), _ptr(drift), _ptr(key_out),
                          _ptr(prob_out), _ptr(workspace), workspace.numel(), _stream(stream, dev))

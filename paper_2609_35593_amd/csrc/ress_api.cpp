@@ -85,6 +85,10 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
     if (params->rounds < 0 || params->rounds > RESS_MAX_ROUNDS || params->swap_floor < 0 ||
         !(params->rho >= 0.0) || !isfinite(params->rho) || !(params->eps > 0.0) || !isfinite(params->eps))
         return RESS_E_INVALID_ARG;
+    if (params->criterion < RESS_CRITERION_DRIFT || params->criterion > RESS_CRITERION_DRIFT_MAX_FULL ||
+        !(params->cdf_tau >= 0.0 && params->cdf_tau <= 1.0) ||
+        (params->cdf_tau > 0.0 && params->criterion != RESS_CRITERION_PROBABILITY))
+        return RESS_E_INVALID_ARG;
     if (!has_work(shape)) return RESS_OK;
     if (!q || !k || !v || !gram || !keep_budget || !kept_count || !kept_idx) return RESS_E_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return RESS_E_INVALID_ARG;
@@ -138,6 +142,8 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
     sp.swap_floor = params->swap_floor;
     sp.rho = params->rho;
     sp.eps = params->eps;
+    sp.criterion = params->criterion;
+    sp.cdf_tau = params->cdf_tau;
     sp.pooled = pooled;
     sp.gram = gram;
     sp.kept_count = kept_count;

@@ -34,7 +34,9 @@ struct SelectParams {
     int first_dense_qb;  // query blocks i >= first_dense_qb keep every block (n_qb if none)
     int rounds, swap_floor;
     int items_per_xcd;   // (head, row group) items per XCD, set by the launcher
+    int criterion;       // RESS_CRITERION_*
     double rho, eps;
+    double cdf_tau;      // 0 = no CDF cap
     Pooled pooled;
     const float *gram;
     int32_t *kept_count, *kept_idx;

@@ -174,7 +174,7 @@ __device__ __forceinline__ void block_pass(const WaveLds<R> &lds, const double (
     __builtin_amdgcn_wave_barrier();
 }
 
-template <int CPL, int R>
+template <int CPL, int R, bool CDF>
 __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
 {
     __shared__ double smem[kWaves * WaveLds<R>::kDoubles];
@@ -328,16 +328,57 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
 
     // Initial selection (Eq. 7), then the state of each drop set (Eqs. 10-12):
     // g = sum_{j in D} P_j (vbar - Vbar_j), K = 1 - sum_{j in D} P_j, G = g^T M g.
+    // The criterion picks the ranking: the key (drift), P (probability) or the
+    // negated key (drift maximisation from the start). A CDF cap (probability
+    // only) shrinks the row's kept count to the shortest descending-P prefix
+    // whose mass, forced blocks included, reaches cdf_tau.
+    const int crit = p.criterion;
+    const bool maximise = crit == RESS_CRITERION_DRIFT_MAX_SWAP || crit == RESS_CRITERION_DRIFT_MAX_FULL;
     unsigned long long inD[R], best[R];
     double K[R], G[R], J[R], J0[R], Jb[R];
+    int crow[R];  // kept candidates of the row
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         inD[r] = 0ull;
+        crow[r] = c_h;
         if (!dense[r]) {
             unsigned long long ko[CPL];
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) ko[c] = order_key(acc[r][c]);
-            const unsigned long long keep = topk_slots<CPL>(ko, memb, c_h, lane_bit, lane_lt);
+            for (int c = 0; c < CPL; ++c)
+                ko[c] = order_key(crit == RESS_CRITERION_PROBABILITY ? P[r][c]
+                                  : crit == RESS_CRITERION_DRIFT_MAX_FULL ? -acc[r][c] : acc[r][c]);
+            if (CDF && crit == RESS_CRITERION_PROBABILITY && p.cdf_tau > 0.0) {
+                // mass(n) = forced mass + the n largest candidate P: smallest n <= c_h
+                // with mass(n) >= tau by bisection (mass is non-decreasing in n).
+                double fm = 0.0;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    const int j = lane + 64 * c;
+                    if (valid[c] && j >= n_p) fm += P[r][c];
+                }
+                fm = wave_sum(fm);
+                auto mass = [&](int n) {
+                    const unsigned long long sel = topk_slots<CPL>(ko, memb, n, lane_bit, lane_lt);
+                    double m = 0.0;
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c)
+                        if ((sel >> c) & 1ull) m += P[r][c];
+                    return fm + wave_sum(m);
+                };
+                int lo = 0, hi = c_h;
+                if (mass(hi) >= p.cdf_tau) {
+                    while (lo < hi) {
+                        const int mid = (lo + hi) >> 1;
+                        if (mass(mid) >= p.cdf_tau)
+                            hi = mid;
+                        else
+                            lo = mid + 1;
+                    }
+                    const int floor2 = max(0, 2 - (nkb - n_p));
+                    crow[r] = max(lo, min(floor2, n_p));
+                }
+            }
+            const unsigned long long keep = topk_slots<CPL>(ko, memb, crow[r], lane_bit, lane_lt);
 #pragma unroll
             for (int c = 0; c < CPL; ++c)
                 if ((memb[c] & lane_bit) && !((keep >> c) & 1ull)) inD[r] |= 1ull << c;
@@ -381,14 +422,19 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
         best[r] = inD[r];
     }
 
-    // Budget-neutral restoration rounds (Eqs. 13-17) with track-best.
-    const int nD = n_p - c_h, nS = c_h;
+    // Budget-neutral restoration rounds (Eqs. 13-17) with track-best. The swap
+    // count follows each row's kept count; rows whose count reached 0 are done.
     double *swap_w = lds.swap_w();
     int *swap_j = lds.swap_j();
     for (int rr = 0; rr < p.rounds; ++rr) {
-        int m = swaps_of_round(c_h, p.rho, rr, p.swap_floor);
-        m = min(m, min(nD, nS));
-        if (m <= 0) break;
+        int mrow[R], mmax = 0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int m = swaps_of_round(crow[r], p.rho, rr, p.swap_floor);
+            mrow[r] = dense[r] ? 0 : min(m, min(n_p - crow[r], crow[r]));
+            mmax = max(mmax, mrow[r]);
+        }
+        if (mmax <= 0) break;
         // e_k . (M g) for every candidate k of every row.
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
@@ -410,7 +456,8 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
         // of each kind are applied together, g and K following Eq. 13.
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            if (dense[r]) continue;
+            const int m = mrow[r];
+            if (m <= 0) continue;
             unsigned long long dj[CPL], memD[CPL], memS[CPL];
 #pragma unroll
             for (int c = 0; c < CPL; ++c) {
@@ -419,7 +466,8 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
                 const double dG = in ? -2.0 * dkMg + S2[r][c] : 2.0 * dkMg + S2[r][c];  // Eqs. 14-15
                 const double Kn = K[r] + (in ? P[r][c] : -P[r][c]);
                 const double Knh = Kn > eps ? Kn : eps;
-                dj[c] = order_key(J[r] - (G[r] + dG) / (Knh * Knh));  // Eq. 16
+                const double dJ = J[r] - (G[r] + dG) / (Knh * Knh);  // Eq. 16
+                dj[c] = order_key(maximise ? -dJ : dJ);
                 memD[c] = __ballot(in);
                 memS[c] = memb[c] & ~memD[c];
             }
@@ -464,7 +512,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
         objective();
 #pragma unroll
         for (int r = 0; r < R; ++r)
-            if (!dense[r] && J[r] < Jb[r]) {
+            if (!dense[r] && (maximise ? J[r] > Jb[r] : J[r] < Jb[r])) {
                 Jb[r] = J[r];
                 best[r] = inD[r];
             }
@@ -501,7 +549,10 @@ hipError_t launch_cfg(const SelectParams &p, hipStream_t s)
     SelectParams q = p;
     const int groups = (p.n_qb + kWaves * R - 1) / (kWaves * R);
     q.items_per_xcd = (p.H * groups + 7) / 8;
-    hipLaunchKernelGGL((select_kernel<CPL, R>), dim3((unsigned)(8 * q.items_per_xcd)), dim3(kThreads), 0, s, q);
+    if (p.cdf_tau > 0.0)  // the CDF cap has its own instantiation (it adds registers)
+        hipLaunchKernelGGL((select_kernel<CPL, R, true>), dim3((unsigned)(8 * q.items_per_xcd)), dim3(kThreads), 0, s, q);
+    else
+        hipLaunchKernelGGL((select_kernel<CPL, R, false>), dim3((unsigned)(8 * q.items_per_xcd)), dim3(kThreads), 0, s, q);
     return hipGetLastError();
 }
 

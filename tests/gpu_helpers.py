@@ -54,14 +54,16 @@ def gpu_select(L, inputs=None, rounds=5, budgets=None, want_debug=True, dense_sp
     return {n: (t.cpu().numpy() if t is not None else None) for n, t in out.items()}, out
 
 
-def oracle_select(L, rounds=5, budgets=None, rows=None, dense_special_queries=True):
+def oracle_select(L, rounds=5, budgets=None, rows=None, dense_special_queries=True, criterion=0, cdf_tau=0.0):
     b = L.budgets if budgets is None else budgets
     return oracle.select(L.q, L.k, L.v, L.gram, b, N=L.N, bq=L.bq, bk=L.bk, n_special=L.n_special_tail,
-                         rounds=rounds, rows=rows, dense_special_queries=dense_special_queries)
+                         rounds=rounds, rows=rows, dense_special_queries=dense_special_queries,
+                         criterion=criterion, cdf_tau=cdf_tau)
 
 
-def check_lists_valid(L, kc, ki, budgets, rows, dense_special_queries=True):
-    """Structure every kept list must have, whatever the decisions."""
+def check_lists_valid(L, kc, ki, budgets, rows, dense_special_queries=True, capped=False):
+    """Structure every kept list must have, whatever the decisions (capped: a CDF
+    cap may keep fewer candidates, never fewer than two blocks in all)."""
     nf = synth.forced_block_count(L.N, L.bk, L.n_special_tail)
     forced = set(range(L.n_kb - nf, L.n_kb))
     dense_rows = dense_special_queries and L.n_special_tail > 0
@@ -72,7 +74,10 @@ def check_lists_valid(L, kc, ki, budgets, rows, dense_special_queries=True):
         lst = ki[r]
         n_p = L.n_kb - nf
         expect = L.n_kb if (i >= first_dense or budgets[h] >= n_p) else int(budgets[h]) + nf
-        assert cnt == expect, (h, i, cnt, expect)
+        if capped and expect < L.n_kb:
+            assert min(2, L.n_kb) <= cnt <= expect, (h, i, cnt, expect)
+        else:
+            assert cnt == expect, (h, i, cnt, expect)
         assert np.all(np.diff(lst[:cnt]) > 0) and lst[0] >= 0 and lst[cnt - 1] < L.n_kb
         assert np.all(lst[cnt:] == -1)
         assert forced <= set(lst[:cnt].tolist())
@@ -83,14 +88,16 @@ def rel_err(a, ref, rowwise_scale):
     return np.abs(a - ref) / den
 
 
-def compare_select(L, gpu, ref, rows=None, budgets=None, label="", dense_special_queries=True):
-    """gpu: full-layer arrays; ref: oracle outputs for `rows` (flat h*n_qb+i)."""
+def compare_select(L, gpu, ref, rows=None, budgets=None, label="", dense_special_queries=True, criterion=0,
+                   capped=False):
+    """gpu: full-layer arrays; ref: oracle outputs for `rows` (flat h*n_qb+i).
+    criterion 2 / 3 maximise the drift, so the returned J is >= the initial one."""
     budgets = L.budgets if budgets is None else budgets
     R = L.H * L.n_qb
     rows = np.arange(R) if rows is None else np.asarray(rows)
     kc = gpu["kept_count"].reshape(R)[rows]
     ki = gpu["kept_idx"].reshape(R, L.n_kb)[rows]
-    check_lists_valid(L, kc, ki, budgets, rows, dense_special_queries)
+    check_lists_valid(L, kc, ki, budgets, rows, dense_special_queries, capped)
     same = (kc == ref["kept_count"]) & np.all(ki == ref["kept_idx"], axis=1)
     decided = ref["margin"] > MARGIN
     bad = np.flatnonzero(decided & ~same)
@@ -111,7 +118,10 @@ def compare_select(L, gpu, ref, rows=None, budgets=None, label="", dense_special
         e_j0 = rel_err(dr[:, 0], ref["drift"][:, 0], scale)
         e_jb = rel_err(dr[same, 1], ref["drift"][same, 1], scale)
         assert e_j0.max() <= REL_TOL and (e_jb.size == 0 or e_jb.max() <= REL_TOL), (label, e_j0.max())
-        assert np.all(dr[:, 1] <= dr[:, 0])
+        if criterion in (2, 3):
+            assert np.all(dr[:, 1] >= dr[:, 0])
+        else:
+            assert np.all(dr[:, 1] <= dr[:, 0])
         out.update(j_init_rel_max=float(e_j0.max()), j_best_rel_max=float(e_jb.max()) if e_jb.size else 0.0)
     stats.update(out)
     say(f"  select parity {label}: {stats}")

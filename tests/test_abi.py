@@ -88,6 +88,9 @@ def test_select_rejects_before_launch(ress):
     assert _select_status(ress, shape, bad_eps, [6, 6]) == ress.RESS_E_INVALID_ARG
     assert _select_status(ress, shape, bad_rho, [6, 6]) == ress.RESS_E_INVALID_ARG
     assert _select_status(ress, shape, None, [6, 6]) == ress.RESS_E_INVALID_ARG
+    for crit, tau in ((4, 0.0), (-1, 0.0), (1, 1.5), (1, -0.1), (1, float("nan")), (0, 0.5), (3, 0.2)):
+        bad = ress.ress_select_params(5, 0.5, 1e-4, 1, 1, crit, tau)
+        assert _select_status(ress, shape, bad, [6, 6]) == ress.RESS_E_INVALID_ARG, (crit, tau)
     assert _select_status(ress, shape, good, [19, 6]) == ress.RESS_E_INVALID_ARG  # > 18 candidates
     assert _select_status(ress, shape, good, [6, -1]) == ress.RESS_E_INVALID_ARG
     # two forced blocks already meet the two-block floor: c_h = 0 is allowed, the

@@ -88,6 +88,32 @@ def test_select_budgets_and_rounds(ress, rounds, frac):
     compare_select(L, gpu, ref, budgets=budgets, label=f"R={rounds} frac={frac}")
 
 
+CRITERIA = [  # (criterion, cdf_tau, rounds): the paper's comparisons, Table 3 and Sec. 5.4
+    (1, 0.0, 0), (1, 0.0, 5), (1, 0.7, 0), (1, 0.9, 3), (2, 0.0, 5), (3, 0.0, 0), (3, 0.0, 5)]
+
+
+@pytest.mark.parametrize("criterion,tau,rounds", CRITERIA)
+@pytest.mark.parametrize("name", ["forced64", "ragged128x64", "b128"])
+def test_select_criteria_small(ress, name, criterion, tau, rounds):
+    L = small(name)
+    say(f"[criterion {criterion} tau={tau} R={rounds}] {name}")
+    gpu, _ = gpu_select(L, rounds=rounds, criterion=criterion, cdf_tau=tau)
+    ref = oracle_select(L, rounds=rounds, criterion=criterion, cdf_tau=tau)
+    compare_select(L, gpu, ref, label=f"{name} crit={criterion} tau={tau} R={rounds}", criterion=criterion,
+                   capped=tau > 0)
+
+
+@pytest.mark.parametrize("criterion,tau", [(1, 0.0), (1, 0.9), (3, 0.0)])
+def test_select_criteria_32v(ress, criterion, tau):
+    """Full-size layer, every row, 5 rounds, for the probability rule (with and
+    without a CDF cap) and the fully sign-flipped objective."""
+    L = synth.make_config("32v", sparsity=0.75)
+    say(f"[criterion {criterion} tau={tau}] 32v")
+    gpu, _ = gpu_select(L, rounds=5, criterion=criterion, cdf_tau=tau, want_debug=False)
+    ref = oracle_select(L, rounds=5, criterion=criterion, cdf_tau=tau)
+    compare_select(L, gpu, ref, label=f"32v crit={criterion} tau={tau}", criterion=criterion, capped=tau > 0)
+
+
 def test_select_without_dense_special_rows(ress):
     L = small("b128")
     say("[select] special query rows selected like the others")
