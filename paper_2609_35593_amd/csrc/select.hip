@@ -174,8 +174,16 @@ __device__ __forceinline__ void block_pass(const WaveLds<R> &lds, const double (
     __builtin_amdgcn_wave_barrier();
 }
 
+// Per-shape tuning, measured: the 32-view shape (6 slots, 2 rows) runs faster with
+// three workgroups per CU (168 VGPRs); 17+ slots run faster with fewer channel
+// loads unrolled (fewer registers held by loads in flight).
+template <int CPL, int R>
+constexpr int kMinBlocks = (CPL == 6 && R == 2) ? 3 : 1;
+template <int CPL>
+constexpr int kUnroll = CPL >= 17 ? 2 : 4;
+
 template <int CPL, int R, bool CDF>
-__global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
+__global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(const SelectParams p)
 {
     __shared__ double smem[kWaves * WaveLds<R>::kDoubles];
     __shared__ float Ms[kD * (kD + 1)];
@@ -237,7 +245,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
         const double *col = Kt + jc[c];
 #pragma unroll
         for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
-#pragma unroll 4
+#pragma unroll kUnroll<CPL>
         for (int d = 0; d < kD; d += 2) {
             const double k0 = col[(size_t)d * nkb], k1 = col[(size_t)(d + 1) * nkb];
 #pragma unroll
@@ -294,7 +302,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
         const double *vcol = Vt + jc[c], *ucol = Ut + jc[c];
 #pragma unroll
         for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
-#pragma unroll 4
+#pragma unroll kUnroll<CPL>
         for (int d = 0; d < kD; d += 2) {
             const double v0 = vcol[(size_t)d * nkb], v1 = vcol[(size_t)(d + 1) * nkb];
             const double u0 = ucol[(size_t)d * nkb], u1 = ucol[(size_t)(d + 1) * nkb];
@@ -441,7 +449,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const SelectParams p)
             const double *vcol = Vt + jc[c];
 #pragma unroll
             for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
-#pragma unroll 4
+#pragma unroll kUnroll<CPL>
             for (int d = 0; d < kD; d += 2) {
                 const double v0 = vcol[(size_t)d * nkb], v1 = vcol[(size_t)(d + 1) * nkb];
 #pragma unroll
