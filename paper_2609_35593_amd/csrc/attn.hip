@@ -25,18 +25,23 @@
 // of key k0 + s/4 and lane i receives channel d0 + i of keys k0..k0+3, which is
 // the transpose the PV product needs.
 //
-// Softmax: base-2 exponentials with the scale folded into one FMA; row sums over
-// the bf16-rounded probabilities (the values the PV product consumes) with
-// packed bf16 dot products. There is no per-half maximum: each row keeps a
-// reference maximum (the largest score seen when it was last set) and forms the
-// probabilities against it directly; only when a half's probability sum leaves
-// [0, 2^20] (a score above the reference by more than 2^20 in probability, or
-// the first keys of the row) is the half redone with its true maximum and O
-// rescaled. Softmax is invariant to the reference, so this changes rounding only.
+// Softmax: base-2 exponentials. Q is multiplied by scale*log2(e) once, when its
+// fragments are loaded (one extra bf16 rounding of Q), so the MFMA accumulators
+// already hold base-2 logits. Row sums run over the bf16-rounded probabilities
+// (the values the PV product consumes) with packed bf16 dot products. There is
+// no per-half maximum: each row keeps a reference and forms the probabilities
+// against it directly; only when a half's probability sum exceeds 2^50 (or the
+// row has no reference yet) is the half redone against its true maximum and O
+// rescaled. A reference within +-40 of the true maximum is rounded to zero, and
+// while every row of a wave has reference zero the wave takes a path whose
+// probabilities are exp2 of the accumulators with no subtraction at all.
+// Softmax is invariant to the reference, so this changes rounding only.
 //
 // Workgroups are numbered so that the 8 XCDs each receive a contiguous range of
 // (head, query block) items: neighbouring query blocks of a head share an XCD
 // and its L2, where their K/V tiles are re-read.
+#include <type_traits>
+
 #include "ress_internal.h"
 
 namespace ress {
@@ -49,7 +54,8 @@ typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr float kSumLimit = 1048576.0f;  // 2^20: largest probability sum a half may reach
+constexpr float kSumLimit = 1125899906842624.0f;  // 2^50: largest probability sum a half may reach
+constexpr float kZeroBand = 40.f;  // references within +-40 (base-2 logits) of the maximum become 0
 
 __device__ __forceinline__ unsigned int bf16_bits(float x)
 {
@@ -94,13 +100,18 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
     const int q0 = i * BQ + wave * 32 + ql;
     const size_t head = (size_t)h * N;
 
+    // Q fragments, pre-multiplied by scale*log2(e) so that scores are base-2 logits.
+    const float c = p.scale_log2;
     bf16x8 qf[4];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-        if (q0 < N)
-            qf[kk] = *reinterpret_cast<const bf16x8 *>(p.q + (head + q0) * kD + kk * 16 + hh * 8);
-        else
+        if (q0 < N) {
+            const bf16x8 x = *reinterpret_cast<const bf16x8 *>(p.q + (head + q0) * kD + kk * 16 + hh * 8);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qf[kk][e] = (__bf16)((float)x[e] * c);
+        } else {
             qf[kk] = bf16x8{};
+        }
     }
 
     int n_ent;  // key blocks to visit
@@ -199,8 +210,8 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
             voff[dh][r] = key * 128 + (((d >> 3) ^ swz(key)) << 4) + (d & 7) * 2;
         }
 
-    const float c = p.scale_log2;
-    float mref = -INFINITY;  // reference maximum of this lane's query row (shared with lane^32)
+    float mref = -INFINITY;  // reference of this lane's query row (shared with lane^32), base-2 logits
+    bool zref = false;       // wave-uniform: every row of the wave has reference 0
     float lrow = 0.f;
     f32x16 acc_o[2];
 #pragma unroll
@@ -248,15 +259,16 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
                 if (key >= nv) s[t][v] = -INFINITY;
             }
     };
-    // Probabilities of sub-tile t (32 keys) of a half against the current
-    // reference; adds the bf16-rounded values to the lane's partial sums.
-    auto probs_part = [&](const f32x16 (&s)[2], bf16x8 (&pb)[2][2], int t, float mc, float &l0,
+    // Probabilities of sub-tile t (32 keys) of a half against reference mc (taken
+    // as 0 when ZERO); adds the bf16-rounded values to the lane's partial sums.
+    auto probs_part = [&](auto zero, const f32x16 (&s)[2], bf16x8 (&pb)[2][2], int t, float mc, float &l0,
                           float &l1) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             float e[8];
 #pragma unroll
-            for (int jj = 0; jj < 8; ++jj) e[jj] = __builtin_amdgcn_exp2f(fmaf(s[t][u * 8 + jj], c, -mc));
+            for (int jj = 0; jj < 8; ++jj)
+                e[jj] = __builtin_amdgcn_exp2f(decltype(zero)::value ? s[t][u * 8 + jj] : s[t][u * 8 + jj] - mc);
             pb[t][u] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
                               (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
 #pragma unroll
@@ -266,13 +278,15 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
             }
         }
     };
-    auto ref_mc = [&]() __attribute__((always_inline)) { return mref == -INFINITY ? 0.f : mref * c; };
+    using general = std::integral_constant<bool, false>;
+    using zero = std::integral_constant<bool, true>;
+    auto ref_mc = [&]() __attribute__((always_inline)) { return mref == -INFINITY ? 0.f : mref; };
     // All probabilities of one half; returns the lane's sum.
     auto probs = [&](const f32x16 (&s)[2], bf16x8 (&pb)[2][2]) __attribute__((always_inline)) -> float {
         const float mc = ref_mc();
         float l0 = 0.f, l1 = 0.f;
-        probs_part(s, pb, 0, mc, l0, l1);
-        probs_part(s, pb, 1, mc, l0, l1);
+        probs_part(general{}, s, pb, 0, mc, l0, l1);
+        probs_part(general{}, s, pb, 1, mc, l0, l1);
         return l0 + l1;
     };
     // Accept the half's probabilities, or redo them against the half's true
@@ -285,14 +299,16 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) tmax = fmaxf(tmax, s[t][v]);
             tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-            const float mnew = fmaxf(mref, tmax);
-            const float alpha = mref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((mref - mnew) * c);
+            float mnew = fmaxf(mref, tmax);
+            if (fabsf(mnew) <= kZeroBand) mnew = 0.f;
+            const float alpha = mref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mref - mnew);
             lrow *= alpha;
 #pragma unroll
             for (int dh = 0; dh < 2; ++dh)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc_o[dh][v] *= alpha;
             mref = mnew;
+            zref = __all(mref == 0.f);
             lh = probs(s, pb);
         }
         lrow += lh;
@@ -300,7 +316,7 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
     // One pipeline step: softmax of the current half (scores sc, nv real keys)
     // beside the score MFMAs of the next half (kt, khf -> sn) and the PV MFMAs
     // of the previous half (probabilities pp, vt, vhf).
-    auto step = [&](f32x16 (&sc)[2], bf16x8 (&pc)[2][2], int nv, f32x16 (&sn)[2], const unsigned char *kt,
+    auto step = [&](auto z, f32x16 (&sc)[2], bf16x8 (&pc)[2][2], int nv, f32x16 (&sn)[2], const unsigned char *kt,
                     int khf, const bf16x8 (&pp)[2][2], const unsigned char *vt, int vhf) __attribute__((always_inline)) {
         if (nv < 64) {
             // A real branch: only partial halves pay for the mask (the empty asm
@@ -311,13 +327,13 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
         // Two scheduling regions. First the score MFMAs of the next half (their
         // results are consumed at the next step) beside the softmax of sub-tile 0,
         // then the PV MFMAs of the previous half beside the softmax of sub-tile 1.
-        const float mc = ref_mc();
+        const float mc = decltype(z)::value ? 0.f : ref_mc();
         float l0 = 0.f, l1 = 0.f;
         qk(kt, khf, sn);
-        probs_part(sc, pc, 0, mc, l0, l1);
+        probs_part(z, sc, pc, 0, mc, l0, l1);
         __builtin_amdgcn_sched_barrier(0);
         pv(vt, vhf, pp);
-        probs_part(sc, pc, 1, mc, l0, l1);
+        probs_part(z, sc, pc, 1, mc, l0, l1);
         const float lh = l0 + l1;
         settle(sc, pc, lh);
     };
@@ -333,15 +349,15 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
     // Tile it (it = 0 .. L-1): K in kc, V in vc; K of tile it+1 in kn; V of tile
     // it-1 in vp. sA holds the scores of (it, half 0), pB the probabilities of
     // (it-1, half 1).
-    auto iter = [&](int it, unsigned char *kc, const unsigned char *kn, const unsigned char *vc,
+    auto iter = [&](auto z, int it, unsigned char *kc, const unsigned char *kn, const unsigned char *vc,
                     unsigned char *vp) __attribute__((always_inline)) {
         fetch_tile(it + 2, jt2);
-        step(sA, pA, half_keys(jt0, 0), sB, kc, 1, pB, vp, 1);
+        step(z, sA, pA, half_keys(jt0, 0), sB, kc, 1, pB, vp, 1);
         wait_vm_all();    // this wave's loads of K(it+1) and V(it) have landed
         __syncthreads();  // ... and every wave's; K(it) and V(it-1) are no longer read
         if (it + 2 < L) dma_tile(kbytes, jt2, kc);
         if (it + 1 < L) dma_tile(vbytes, jt1, vp);
-        step(sB, pB, half_keys(jt0, 1), sA, kn, 0, pA, vc, 0);
+        step(z, sB, pB, half_keys(jt0, 1), sA, kn, 0, pA, vc, 0);
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
             jt0[e] = jt1[e];
@@ -362,9 +378,11 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
         qk(k_lds0, 0, sA);
         int it = 0;
         for (;;) {
-            iter(it, k_lds0, k_lds1, v_lds0, v_lds1);
+            if (zref) iter(zero{}, it, k_lds0, k_lds1, v_lds0, v_lds1);
+            else iter(general{}, it, k_lds0, k_lds1, v_lds0, v_lds1);
             if (++it >= L) break;
-            iter(it, k_lds1, k_lds0, v_lds1, v_lds0);
+            if (zref) iter(zero{}, it, k_lds1, k_lds0, v_lds1, v_lds0);
+            else iter(general{}, it, k_lds1, k_lds0, v_lds1, v_lds0);
             if (++it >= L) break;
         }
         // PV of the last half; its tile sits in V slot (L-1) % 2.
