@@ -54,8 +54,10 @@ typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr float kSumLimit = 1125899906842624.0f;  // 2^50: largest probability sum a half may reach
-constexpr float kZeroBand = 40.f;  // references within +-40 (base-2 logits) of the maximum become 0
+constexpr float kSumLimit = 0x1p50f;  // largest probability sum a half may reach
+constexpr float kTiny = 0x1p-100f;    // a row whose running sum is below this has no usable reference
+constexpr float kZeroBand = 40.f;     // references within +-40 (base-2 logits) become 0
+constexpr float kStartBand = 24.f;    // first-half maxima a wave may have to start with reference 0
 
 __device__ __forceinline__ unsigned int bf16_bits(float x)
 {
@@ -100,19 +102,27 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
     const int q0 = i * BQ + wave * 32 + ql;
     const size_t head = (size_t)h * N;
 
-    // Q fragments, pre-multiplied by scale*log2(e) so that scores are base-2 logits.
+    // Q fragments, pre-multiplied by scale*log2(e) so that scores are base-2 logits,
+    // unless the wave's first scores show logits beyond kStartBand (then unscaled).
     const float c = p.scale_log2;
     bf16x8 qf[4];
+    auto load_q = [&](bool scaled) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-        if (q0 < N) {
-            const bf16x8 x = *reinterpret_cast<const bf16x8 *>(p.q + (head + q0) * kD + kk * 16 + hh * 8);
+        for (int kk = 0; kk < 4; ++kk) {
+            if (q0 < N) {
+                const bf16x8 x = *reinterpret_cast<const bf16x8 *>(p.q + (head + q0) * kD + kk * 16 + hh * 8);
+                if (scaled) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) qf[kk][e] = (__bf16)((float)x[e] * c);
-        } else {
-            qf[kk] = bf16x8{};
+                    for (int e = 0; e < 8; ++e) qf[kk][e] = (__bf16)((float)x[e] * c);
+                } else {
+                    qf[kk] = x;
+                }
+            } else {
+                qf[kk] = bf16x8{};
+            }
         }
-    }
+    };
+    load_q(true);
 
     int n_ent;  // key blocks to visit
     const int32_t *list = nullptr;
@@ -210,8 +220,9 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
             voff[dh][r] = key * 128 + (((d >> 3) ^ swz(key)) << 4) + (d & 7) * 2;
         }
 
-    float mref = -INFINITY;  // reference of this lane's query row (shared with lane^32), base-2 logits
-    bool zref = false;       // wave-uniform: every row of the wave has reference 0
+    float mref = 0.f;   // reference of this lane's query row (shared with lane^32), base-2 logits
+    bool zref = true;   // wave-uniform: every row has reference 0 (Q then is pre-scaled)
+    float cw = 1.f;     // wave-uniform: base-2 logit per unit score (1 for pre-scaled Q, else c)
     float lrow = 0.f;
     f32x16 acc_o[2];
 #pragma unroll
@@ -259,16 +270,19 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
                 if (key >= nv) s[t][v] = -INFINITY;
             }
     };
-    // Probabilities of sub-tile t (32 keys) of a half against reference mc (taken
-    // as 0 when ZERO); adds the bf16-rounded values to the lane's partial sums.
-    auto probs_part = [&](auto zero, const f32x16 (&s)[2], bf16x8 (&pb)[2][2], int t, float mc, float &l0,
+    // Probabilities of sub-tile t (32 keys) of a half, exp2(s) when every row has
+    // reference 0 (Z), else exp2(s * cw - mref); adds the bf16-rounded values to
+    // the lane's partial sums.
+    auto probs_part = [&](auto z, const f32x16 (&s)[2], bf16x8 (&pb)[2][2], int t, float &l0,
                           float &l1) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             float e[8];
 #pragma unroll
-            for (int jj = 0; jj < 8; ++jj)
-                e[jj] = __builtin_amdgcn_exp2f(decltype(zero)::value ? s[t][u * 8 + jj] : s[t][u * 8 + jj] - mc);
+            for (int jj = 0; jj < 8; ++jj) {
+                const float x = s[t][u * 8 + jj];
+                e[jj] = __builtin_amdgcn_exp2f(decltype(z)::value ? x : fmaf(x, cw, -mref));
+            }
             pb[t][u] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
                               (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
 #pragma unroll
@@ -278,37 +292,41 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
             }
         }
     };
+    // Tile-loop variants: every row's reference is 0 (zero), or per-row references (general).
     using general = std::integral_constant<bool, false>;
     using zero = std::integral_constant<bool, true>;
-    auto ref_mc = [&]() __attribute__((always_inline)) { return mref == -INFINITY ? 0.f : mref; };
-    // All probabilities of one half; returns the lane's sum.
+    // All probabilities of one half against the current references; returns the lane's sum.
     auto probs = [&](const f32x16 (&s)[2], bf16x8 (&pb)[2][2]) __attribute__((always_inline)) -> float {
-        const float mc = ref_mc();
         float l0 = 0.f, l1 = 0.f;
-        probs_part(general{}, s, pb, 0, mc, l0, l1);
-        probs_part(general{}, s, pb, 1, mc, l0, l1);
+        probs_part(general{}, s, pb, 0, l0, l1);
+        probs_part(general{}, s, pb, 1, l0, l1);
         return l0 + l1;
     };
-    // Accept the half's probabilities, or redo them against the half's true
-    // maximum (rescaling O and the running sum) when they left the safe range.
-    auto settle = [&](const f32x16 (&s)[2], bf16x8 (&pb)[2][2], float lh) __attribute__((always_inline)) {
-        if (__any(!(lh <= kSumLimit) || mref == -INFINITY)) {
+    // Accept the half's probabilities, or redo them against a new reference
+    // (rescaling O and the running sum) when the half's sum exceeds kSumLimit,
+    // the row still has no mass above kTiny, or (zero variant) a row of the wave
+    // already left reference 0 earlier in this tile.
+    auto settle = [&](auto z, const f32x16 (&s)[2], bf16x8 (&pb)[2][2], float lh) __attribute__((always_inline)) {
+        constexpr bool Z = decltype(z)::value;
+        if (__any(!(lh <= kSumLimit) || lrow + lh < kTiny || (Z && mref != 0.f))) {
             float tmax = -INFINITY;
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) tmax = fmaxf(tmax, s[t][v]);
-            tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-            float mnew = fmaxf(mref, tmax);
+            tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * cw;
+            // The reference only rises, except while the row has no usable mass yet.
+            float mnew = lrow < kTiny ? tmax : fmaxf(mref, tmax);
+            if (tmax == -INFINITY) mnew = mref;  // a fully masked half says nothing
             if (fabsf(mnew) <= kZeroBand) mnew = 0.f;
-            const float alpha = mref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mref - mnew);
+            const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
             lrow *= alpha;
 #pragma unroll
             for (int dh = 0; dh < 2; ++dh)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc_o[dh][v] *= alpha;
             mref = mnew;
-            zref = __all(mref == 0.f);
+            if (Z) zref = __all(mref == 0.f);
             lh = probs(s, pb);
         }
         lrow += lh;
@@ -327,15 +345,14 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
         // Two scheduling regions. First the score MFMAs of the next half (their
         // results are consumed at the next step) beside the softmax of sub-tile 0,
         // then the PV MFMAs of the previous half beside the softmax of sub-tile 1.
-        const float mc = decltype(z)::value ? 0.f : ref_mc();
         float l0 = 0.f, l1 = 0.f;
         qk(kt, khf, sn);
-        probs_part(z, sc, pc, 0, mc, l0, l1);
+        probs_part(z, sc, pc, 0, l0, l1);
         __builtin_amdgcn_sched_barrier(0);
         pv(vt, vhf, pp);
-        probs_part(z, sc, pc, 1, mc, l0, l1);
+        probs_part(z, sc, pc, 1, l0, l1);
         const float lh = l0 + l1;
-        settle(sc, pc, lh);
+        settle(z, sc, pc, lh);
     };
 
     f32x16 sA[2], sB[2];
@@ -376,7 +393,25 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
         wait_vm_all();
         __syncthreads();
         qk(k_lds0, 0, sA);
+        {
+            // Start with reference 0 only if every row's first logits lie within
+            // kStartBand; otherwise use unscaled Q (exact scores) from the start.
+            float m0 = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) m0 = fmaxf(m0, sA[t][v]);
+            m0 = fmaxf(m0, __shfl_xor(m0, 32));
+            zref = __all(fabsf(m0) <= kStartBand);
+            if (!zref) {
+                load_q(false);
+                cw = c;
+                qk(k_lds0, 0, sA);
+            }
+        }
         int it = 0;
+        // A wave leaves the zero variant (for good) when a row's reference leaves 0;
+        // its Q stays pre-scaled (cw = 1), so every score of a row has one form.
         for (;;) {
             if (zref) iter(zero{}, it, k_lds0, k_lds1, v_lds0, v_lds1);
             else iter(general{}, it, k_lds0, k_lds1, v_lds0, v_lds1);

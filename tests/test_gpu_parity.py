@@ -138,6 +138,44 @@ def test_zero_sparsity_sparse_equals_dense(ress):
     assert torch.equal(o_s, o_d)
 
 
+
+def _logit_range_layer():
+    """Four heads whose query rows sit at different logit ranges: head 0 as drawn
+    (natural logits up to ~15), head 1 with every query scaled by 6 (up to ~100),
+    head 2 with every fifth query scaled by 6 (waves that mix both ranges), head 3
+    with keys along a shared direction and queries against it (every row's
+    largest logit near -36, about -52 in base 2)."""
+    import dataclasses
+
+    L = synth.make_layer(2, 700, 5, H=4, block=128, sparsity=0.5, seed=31, name="logit-ranges")
+    q = synth.bf16_bits_to_f32(L.q).astype(np.float64)
+    k = synth.bf16_bits_to_f32(L.k).astype(np.float64)
+    q[1] *= 6.0
+    q[2, ::5] *= 6.0
+    u = np.full(64, 1.0 / 8.0)  # unit vector
+    k[3] = 0.25 * k[3] + 4.0 * u
+    q[3] = 0.25 * q[3] - 80.0 * u
+    return dataclasses.replace(L, q=synth.f32_to_bf16_bits(q.astype(np.float32)),
+                               k=synth.f32_to_bf16_bits(k.astype(np.float32)))
+
+
+def test_attention_logit_ranges(ress):
+    """Dense and sparse attention where rows leave the band in which the kernel
+    forms probabilities without a reference subtraction, at the same tolerance."""
+    import torch
+
+    L = _logit_range_layer()
+    say(f"[logit ranges] H={L.H} N={L.N}")
+    inputs = device_inputs(L)
+    q, k, v, _ = inputs
+    hs, ts = _all_tokens(L)
+    o = ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk)
+    compare_attn(L, o, hs, ts, label="logit ranges dense")
+    gpu, dev = gpu_select(L, inputs)
+    o = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk)
+    torch.cuda.synchronize()
+    compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label="logit ranges sparse")
+
 # ------------------------------------------------------------------ the five workloads
 
 
