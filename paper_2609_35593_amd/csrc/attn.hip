@@ -25,16 +25,18 @@
 // of key k0 + s/4 and lane i receives channel d0 + i of keys k0..k0+3, which is
 // the transpose the PV product needs.
 //
-// Softmax: base-2 exponentials. Q is multiplied by scale*log2(e) once, when its
-// fragments are loaded (one extra bf16 rounding of Q), so the MFMA accumulators
-// already hold base-2 logits. Row sums run over the bf16-rounded probabilities
+// Softmax: base-2 exponentials; row sums over the bf16-rounded probabilities
 // (the values the PV product consumes) with packed bf16 dot products. There is
-// no per-half maximum: each row keeps a reference and forms the probabilities
-// against it directly; only when a half's probability sum exceeds 2^50 (or the
-// row has no reference yet) is the half redone against its true maximum and O
-// rescaled. A reference within +-40 of the true maximum is rounded to zero, and
-// while every row of a wave has reference zero the wave takes a path whose
-// probabilities are exp2 of the accumulators with no subtraction at all.
+// no per-half maximum: every row starts with reference 0 and forms its
+// probabilities against its reference; only when a half's sum exceeds 2^50, or
+// the row's running sum is still below 2^-100, is the half redone against its
+// true maximum (a result within +-40 of 0 is rounded to 0) and O rescaled.
+// While every row of a wave has reference 0, the wave runs a copy of the tile
+// loop whose probabilities are exp2 of the score accumulators with nothing
+// else: Q is multiplied by scale*log2(e) when its fragments are loaded (one extra
+// bf16 rounding of Q), so the accumulators are base-2 logits. A wave whose first
+// 64 scores reach beyond +-24 in some row reloads Q unscaled instead, so large
+// logits are formed exactly; either way every score of a row has one form.
 // Softmax is invariant to the reference, so this changes rounding only.
 //
 // Workgroups are numbered so that the 8 XCDs each receive a contiguous range of

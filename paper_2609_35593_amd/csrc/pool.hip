@@ -1,18 +1,24 @@
 // Block mean pooling of Q, K and V (the coarse block grid of Sec. 3, step (1)),
 // plus U_j = M_h Vbar_j for the drift scores (Eq. 9).
 //
-// One workgroup per (head, block). Each thread streams 16-byte rows segments of
-// the block (8 channels of one token); partial sums are float64, which holds the
-// sum of bf16 values of a block exactly, so the mean (one division) equals the
-// float64 mean computed in any order. This pass is the only part of the
-// selection that reads Q, K, V from HBM.
+// One wave per pooled block; a workgroup holds 4 waves that pool 4 consecutive
+// blocks of the same head and tensor, so the channel-major outputs are written
+// 4 blocks (32 bytes) at a time and, for V, the head's M_h is staged in LDS once
+// for 4 blocks. Lane l streams the 16-byte chunk l/8 (channels 8(l/8)..+7) of
+// tokens l%8, l%8 + 8, ...: every load instruction of a wave covers 8 whole
+// 128-byte token rows, and a block is one batch of independent loads. Partial
+// sums are float64; the 8 lanes of a chunk are combined with a fixed butterfly,
+// after which lane t holds channel t. A float64 sum of bf16 values is exact
+// unless the block's values span more than about 2^40 in magnitude, so the
+// means equal the float64 means computed in any order. This pass is the only
+// part of the selection that reads Q, K, V from HBM.
 #include "ress_internal.h"
 
 namespace ress {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTokLanes = kThreads / 8;  // threads that share one 8-channel chunk
+constexpr int kWaves = kThreads / 64;  // blocks per workgroup
 
 __device__ __forceinline__ void accum_bf16x8(double (&acc)[8], uint4 w)
 {
@@ -24,68 +30,99 @@ __device__ __forceinline__ void accum_bf16x8(double (&acc)[8], uint4 w)
     }
 }
 
-// Sums rows [lo, lo+cnt) of x[h] into red[kTokLanes][64], then returns (to the
-// first 64 threads) the block mean of channel threadIdx.x.
-__device__ __forceinline__ double block_mean(const uint16_t *__restrict__ x, size_t row0, int cnt,
-                                             int maxb, double *red)
+// Mean over rows [row0, row0 + cnt) (cnt <= 128) of x[.][64]; lane t of the wave
+// returns channel t.
+__device__ __forceinline__ double wave_block_mean(const uint16_t *__restrict__ x, size_t row0, int cnt)
 {
-    const int t = threadIdx.x, ch = t & 7, sub = t >> 3;
+    const int lane = threadIdx.x & 63, chunk = lane >> 3, sub = lane & 7;
     double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    uint4 w[4];
+    uint4 w[16];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int tok = sub + r * kTokLanes;
-        w[r] = (r * kTokLanes < maxb && tok < cnt)
-                   ? *reinterpret_cast<const uint4 *>(x + (row0 + tok) * kD + ch * 8)
-                   : make_uint4(0, 0, 0, 0);
+    for (int r = 0; r < 16; ++r) {
+        const int tok = sub + 8 * r;
+        w[r] = tok < cnt ? *reinterpret_cast<const uint4 *>(x + (row0 + tok) * kD + chunk * 8)
+                         : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) accum_bf16x8(acc, w[r]);
+    for (int r = 0; r < 16; ++r) accum_bf16x8(acc, w[r]);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) red[sub * kD + ch * 8 + e] = acc[e];
-    __syncthreads();
-    double mean = 0.0;
-    if (t < kD) {
-        double s = 0.0;
-        for (int r = 0; r < kTokLanes; ++r) s += red[r * kD + t];
-        mean = s / (double)cnt;
-    }
-    __syncthreads();
-    return mean;
+    for (int o = 1; o <= 4; o <<= 1)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o);
+    // Every lane of a chunk now holds the chunk's 8 channel sums; lane t keeps
+    // channel t = 8 * chunk + (t & 7).
+    double s = acc[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) s = (sub == e) ? acc[e] : s;
+    return s / (double)cnt;
 }
 
 __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
 {
-    __shared__ double red[kTokLanes * kD];
-    __shared__ double vmean[kD];
-    __shared__ float Ms[kD * (kD + 1)];
-    const int t = threadIdx.x;
-    const int nq = p.H * p.n_qb;
-    if ((int)blockIdx.x < nq) {
-        const int h = blockIdx.x / p.n_qb, i = blockIdx.x % p.n_qb;
+    __shared__ float Ms[kD * (kD + 1)];       // M_h, padded rows (V workgroups)
+    __shared__ double vb[kWaves][kD];         // each wave's Vbar_j
+    __shared__ double tile[2][kD][kWaves];    // channel-major outputs of the 4 blocks
+    const int t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int gq = (p.n_qb + kWaves - 1) / kWaves, gk = (p.n_kb + kWaves - 1) / kWaves;
+    const int per_head = gq + 2 * gk;
+    const int h = blockIdx.x / per_head, g = blockIdx.x % per_head;
+
+    if (g < gq) {  // query blocks: row-major output only
+        const int i = g * kWaves + wave;
+        if (i >= p.n_qb) return;
         const int lo = i * p.bq, cnt = min(p.bq, p.N - lo);
-        const double m = block_mean(p.q, (size_t)h * p.N + lo, cnt, p.bq, red);
-        if (t < kD) p.out.qbar[((size_t)h * p.n_qb + i) * kD + t] = m;
+        p.out.qbar[((size_t)h * p.n_qb + i) * kD + lane] = wave_block_mean(p.q, (size_t)h * p.N + lo, cnt);
         return;
     }
-    const int b = blockIdx.x - nq;
-    const int h = b / p.n_kb, j = b % p.n_kb;
-    const int lo = j * p.bk, cnt = min(p.bk, p.N - lo);
-    const float *Mh = p.gram + (size_t)h * kD * kD;
-    for (int e = t; e < kD * kD; e += kThreads) Ms[(e >> 6) * (kD + 1) + (e & 63)] = Mh[e];
-    const double km = block_mean(p.k, (size_t)h * p.N + lo, cnt, p.bk, red);
-    const double vm = block_mean(p.v, (size_t)h * p.N + lo, cnt, p.bk, red);
-    if (t < kD) {
-        p.out.kbarT[((size_t)h * kD + t) * p.n_kb + j] = km;
-        p.out.vbar[((size_t)h * p.n_kb + j) * kD + t] = vm;
-        p.out.vbarT[((size_t)h * kD + t) * p.n_kb + j] = vm;
-        vmean[t] = vm;
+    const bool is_v = g >= gq + gk;
+    const int j0 = (is_v ? g - gq - gk : g - gq) * kWaves;
+    const int j = j0 + wave;
+    const int nb = min(kWaves, p.n_kb - j0);  // blocks of this workgroup
+    constexpr int MPT = kD * kD / 4 / kThreads;  // float4 pieces of M_h per thread
+    float4 mreg[MPT];
+    if (is_v) {  // issued before the block loads, stored to LDS after them
+        const float4 *Mh = reinterpret_cast<const float4 *>(p.gram + (size_t)h * kD * kD);
+#pragma unroll
+        for (int u = 0; u < MPT; ++u) mreg[u] = Mh[u * kThreads + t];
+    }
+    if (j < p.n_kb) {
+        const int lo = j * p.bk, cnt = min(p.bk, p.N - lo);
+        const double mean = wave_block_mean(is_v ? p.v : p.k, (size_t)h * p.N + lo, cnt);
+        if (is_v) {
+            p.out.vbar[((size_t)h * p.n_kb + j) * kD + lane] = mean;
+            vb[wave][lane] = mean;
+        }
+        tile[0][lane][wave] = mean;
+    }
+    if (is_v) {  // M_h row r, column c at r * 65 + c
+#pragma unroll
+        for (int u = 0; u < MPT; ++u) {
+            const int e = 4 * (u * kThreads + t), r = e >> 6, c = e & 63;
+            float *dst = Ms + r * (kD + 1) + c;
+            dst[0] = mreg[u].x;
+            dst[1] = mreg[u].y;
+            dst[2] = mreg[u].z;
+            dst[3] = mreg[u].w;
+        }
     }
     __syncthreads();
-    if (t < kD) {
+    if (is_v && j < p.n_kb) {  // U_j = M_h Vbar_j, lane t <-> output channel t
         double u = 0.0;
-        for (int c = 0; c < kD; ++c) u = fma((double)Ms[t * (kD + 1) + c], vmean[c], u);
-        p.out.uT[((size_t)h * kD + t) * p.n_kb + j] = u;
+        for (int c = 0; c < kD; ++c) u = fma((double)Ms[lane * (kD + 1) + c], vb[wave][c], u);
+        tile[1][lane][wave] = u;
+    }
+    __syncthreads();
+    // Channel-major outputs: thread (row, w) writes block j0 + w of channel row.
+    const int row = t >> 2, w = t & 3;
+    if (w < nb) {
+        const size_t off = ((size_t)h * kD + row) * p.n_kb + j0 + w;
+        if (is_v) {
+            p.out.vbarT[off] = tile[0][row][w];
+            p.out.uT[off] = tile[1][row][w];
+        } else {
+            p.out.kbarT[off] = tile[0][row][w];
+        }
     }
 }
 
@@ -93,7 +130,8 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
 
 hipError_t launch_pool(const PoolParams &p, hipStream_t s)
 {
-    const long long blocks = (long long)p.H * (p.n_qb + p.n_kb);
+    const int gq = (p.n_qb + kWaves - 1) / kWaves, gk = (p.n_kb + kWaves - 1) / kWaves;
+    const long long blocks = (long long)p.H * (gq + 2 * gk);
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(pool_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
     return hipGetLastError();
