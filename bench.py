@@ -44,6 +44,7 @@ def parse():
     ap.add_argument("--bk", type=int, default=None, help="key block size (default: the workload's)")
     ap.add_argument("--no-flush", action="store_true", help="skip the cache-flushed secondary timing")
     ap.add_argument("--no-criteria", action="store_true", help="skip the per-criterion drift report")
+    ap.add_argument("--no-masking", action="store_true", help="skip the single-block masking report")
     ap.add_argument("--rounds", type=int, default=5)
     ap.add_argument("--dense-steps", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
@@ -184,6 +185,47 @@ def criteria_report(ress, L, q, k, v, gram, o_dense, stream):
     return rep
 
 
+def masking_report(ress, L, q, k, v, gram, stream):
+    """Sec. 2's test of the probability assumption (Fig. 2) on this synthetic layer:
+    mask one candidate key block at a time (every query block attends to all other
+    blocks, float32 outputs from this library's kernel) and measure the change
+    ||W_O (O_masked - O_dense)|| over each query block's tokens; then, per selected
+    row, the Spearman correlation of that change with the pooled probability P_ij,
+    the drift score s_ij (Eq. 6) and the ranking key s_ij / (1 - P_ij) (Eq. 7) over
+    the row's candidates. Dense special rows are left out."""
+    import torch
+
+    from paper_2609_35593_amd import masking
+    import synth
+
+    t0 = time.time()
+    n_qb, n_kb = L.n_qb, L.n_kb
+    nf = synth.forced_block_count(L.N, L.bk, L.n_special_tail)
+    cand = np.arange(n_kb - nf)
+    sel = ress.ress_select(q, k, v, gram, L.budgets, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                           want_debug=True, stream=stream)
+    P = sel["prob"].cpu().numpy()[:, :, cand]
+    key = sel["key"].cpu().numpy()[:, :, cand]
+    s = key * np.maximum(1.0 - P, 1e-4)
+    change = masking.block_masking_change(q, k, v, gram, bq=L.bq, bk=L.bk, blocks=cand, stream=stream)
+    torch.cuda.synchronize()
+    first_special = (L.N - L.n_special_tail) // L.bq if L.n_special_tail > 0 else n_qb
+    rows = (slice(None), slice(0, first_special))
+    out = {"rows": int(L.H * first_special), "candidates": int(len(cand))}
+    for name, x in (("probability", P), ("drift_score", s), ("ranking_key", key)):
+        r = masking.spearman_rows(change[rows], x[rows])
+        r = r[np.isfinite(r)]
+        out[name] = {"mean": round(float(r.mean()), 4), "median": round(float(np.median(r)), 4),
+                     "p10": round(float(np.percentile(r, 10)), 4), "min": round(float(r.min()), 4)}
+    rp = masking.spearman_rows(change[rows], P[rows])
+    rk = masking.spearman_rows(change[rows], key[rows])
+    out["key_above_probability_frac"] = round(float(np.mean(rk > rp)), 4)
+    out["per_head_mean"] = {"probability": [round(float(np.nanmean(rp[h])), 3) for h in range(L.H)],
+                            "ranking_key": [round(float(np.nanmean(rk[h])), 3) for h in range(L.H)]}
+    out["seconds"] = round(time.time() - t0, 1)
+    return out
+
+
 def copy_calibration():
     import torch
 
@@ -290,6 +332,7 @@ def main():
 
     ceilings = measured_ceilings(torch, dev)
     criteria = None if args.no_criteria else criteria_report(ress, L, q, k, v, gram, od, stream)
+    mask_rep = None if args.no_masking else masking_report(ress, L, q, k, v, gram, stream)
 
     kc_h, ki_h, dr = kc.cpu().numpy(), ki.cpu().numpy(), drift.cpu().numpy().reshape(-1, 2)
     flops_kept, kept_tiles = kept_flops(L, kc_h, ki_h)
@@ -359,6 +402,7 @@ def main():
             "measured_ceilings": ceilings,
             "cache_flushed": flushed,
             "criteria_same_budget": criteria,
+            "single_block_masking": mask_rep,
             "input_generation_s": round(gen_s, 1),
         },
     }

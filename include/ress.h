@@ -148,6 +148,16 @@ int ress_sparse_attn(const ress_shape *shape, const void *q, const void *k, cons
                      const int32_t *kept_count, const int32_t *kept_idx, float scale, void *o,
                      hipStream_t stream);
 
+/* ress_sparse_attn with a float32 output (device float32 [H][N][D], 16-byte
+ * aligned, must not alias q, k, v): the same kernels, only the final
+ * normalised O is stored unrounded. Differences between two such outputs
+ * resolve changes far below the bf16 output's resolution, e.g. the output
+ * change caused by masking one key block, the reference measurement of Sec. 2
+ * (Fig. 2). */
+int ress_sparse_attn_out_f32(const ress_shape *shape, const void *q, const void *k, const void *v,
+                             const int32_t *kept_count, const int32_t *kept_idx, float scale, float *o,
+                             hipStream_t stream);
+
 /* Dense attention, the same computation over every key block of every row
  * (the baseline the paper compares against, Table S6). */
 int ress_dense_attn(const ress_shape *shape, const void *q, const void *k, const void *v,

@@ -228,3 +228,52 @@ def attn_tokens(q, k, v, *, N, bq, bk, scale, sel_h, sel_t, kept_count=None, kep
     ki = None if kept_idx is None else _c(kept_idx, np.int32).reshape(-1)
     _L().ro_attn_tokens(H, N, D, bq, bk, q, k, v, float(scale), kc, ki, len(sh), sh, st, out)
     return out
+
+
+def block_masking_change(q, k, v, gram, *, N, bq, bk, scale, h, i, blocks):
+    """The reference measurement of Sec. 2 (Fig. 2) for query block i of head h:
+    for each key block j in `blocks`, mask only block j and take the change in what
+    attention writes into the residual stream, the Euclidean norm over the query
+    block's tokens of W_O^h (O_t(B minus j) - O_t(B)), with ||W_O^h x||^2 = x^T M_h x.
+    Returns float64 [len(blocks)]."""
+    q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    H, _, D = q.shape
+    n_qb, n_kb = (N + bq - 1) // bq, (N + bk - 1) // bk
+    toks = np.arange(i * bq, min((i + 1) * bq, N), dtype=np.int32)
+    heads = np.full(len(toks), h, np.int32)
+    dense = attn_tokens(q, k, v, N=N, bq=bq, bk=bk, scale=scale, sel_h=heads, sel_t=toks)
+    M = np.asarray(gram[h], dtype=np.float64)
+    out = np.empty(len(blocks))
+    for n, j in enumerate(blocks):
+        keep = [b for b in range(n_kb) if b != j]
+        kc = np.zeros((H, n_qb), np.int32)
+        ki = np.full((H, n_qb, n_kb), -1, np.int32)
+        kc[h, i] = len(keep)
+        ki[h, i, :len(keep)] = keep
+        d = attn_tokens(q, k, v, N=N, bq=bq, bk=bk, scale=scale, sel_h=heads, sel_t=toks, kept_count=kc,
+                        kept_idx=ki) - dense
+        out[n] = np.sqrt(max(float(np.einsum("td,de,te->", d, M, d)), 0.0))
+    return out
+
+
+def spearman(a, b) -> float:
+    """Spearman rank correlation: the Pearson correlation of the two rankings,
+    tied values sharing their average rank (nan if either ranking is constant)."""
+    def ranks(x):
+        x = np.asarray(x, dtype=np.float64)
+        order = np.argsort(x, kind="mergesort")
+        sx = x[order]
+        r = np.empty(len(x))
+        s = 0
+        while s < len(x):
+            e = s
+            while e + 1 < len(x) and sx[e + 1] == sx[s]:
+                e += 1
+            r[order[s:e + 1]] = 0.5 * (s + e)
+            s = e + 1
+        return r
+    ra, rb = ranks(a), ranks(b)
+    ra -= ra.mean()
+    rb -= rb.mean()
+    den = np.sqrt(np.dot(ra, ra) * np.dot(rb, rb))
+    return float(np.dot(ra, rb) / den) if den > 0 else float("nan")

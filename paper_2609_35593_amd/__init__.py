@@ -61,6 +61,8 @@ def _load():
     L.ress_select.restype = i
     L.ress_sparse_attn.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, f, vp, vp]
     L.ress_sparse_attn.restype = i
+    L.ress_sparse_attn_out_f32.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, f, vp, vp]
+    L.ress_sparse_attn_out_f32.restype = i
     L.ress_dense_attn.argtypes = [C.POINTER(ress_shape), vp, vp, vp, f, vp, vp]
     L.ress_dense_attn.restype = i
     return L
@@ -149,9 +151,7 @@ def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail:
     return dict(kept_count=kept_count, kept_idx=kept_idx, drift=drift, key=key_out, prob=prob_out)
 
 
-def ress_sparse_attn(q, k, v, kept_count, kept_idx, *, bq: int, bk: int, n_special_tail: int = 0,
-                     scale: float | None = None, out=None, stream=None):
-    """Block-sparse attention over the kept key blocks (see include/ress.h)."""
+def _sparse_call(fn, name, q, k, v, kept_count, kept_idx, bq, bk, n_special_tail, scale, out, out_dtype, stream):
     _check_qkv(q, k, v)
     H, N, D = q.shape
     shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
@@ -162,13 +162,29 @@ def ress_sparse_attn(q, k, v, kept_count, kept_idx, *, bq: int, bk: int, n_speci
     if kept_count.numel() != H * n_qb or kept_idx.numel() != H * n_qb * n_kb:
         raise ValueError("kept_count must be [H][n_qb] and kept_idx [H][n_qb][n_kb]")
     if out is None:
-        out = torch.empty_like(q)
+        out = torch.empty(q.shape, dtype=out_dtype, device=q.device)
+    if not (out.is_cuda and out.dtype == out_dtype and out.is_contiguous() and tuple(out.shape) == tuple(q.shape)):
+        raise ValueError(f"out must be a contiguous CUDA {out_dtype} tensor shaped like q")
     scale = 1.0 / math.sqrt(D) if scale is None else scale
-    st = lib.ress_sparse_attn(C.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(kept_count), _ptr(kept_idx),
-                              float(scale), _ptr(out), _stream(stream, q.device))
+    st = fn(C.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(kept_count), _ptr(kept_idx), float(scale), _ptr(out),
+            _stream(stream, q.device))
     if st != RESS_OK:
-        raise RessError(st, "ress_sparse_attn")
+        raise RessError(st, name)
     return out
+
+
+def ress_sparse_attn(q, k, v, kept_count, kept_idx, *, bq: int, bk: int, n_special_tail: int = 0,
+                     scale: float | None = None, out=None, stream=None):
+    """Block-sparse attention over the kept key blocks (see include/ress.h)."""
+    return _sparse_call(lib.ress_sparse_attn, "ress_sparse_attn", q, k, v, kept_count, kept_idx, bq, bk,
+                        n_special_tail, scale, out, torch.bfloat16, stream)
+
+
+def ress_sparse_attn_out_f32(q, k, v, kept_count, kept_idx, *, bq: int, bk: int, n_special_tail: int = 0,
+                             scale: float | None = None, out=None, stream=None):
+    """ress_sparse_attn with a float32 output (see include/ress.h)."""
+    return _sparse_call(lib.ress_sparse_attn_out_f32, "ress_sparse_attn_out_f32", q, k, v, kept_count, kept_idx,
+                        bq, bk, n_special_tail, scale, out, torch.float32, stream)
 
 
 def ress_dense_attn(q, k, v, *, bq: int, bk: int, n_special_tail: int = 0, scale: float | None = None,

@@ -429,7 +429,18 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
     // Each lane summed half of its row's keys; lanes l and l^32 share the row.
     const float ltot = lrow + __shfl_xor(lrow, 32);
     const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-    if (q0 < N) {
+    if (q0 < N && p.o32) {
+        float *orow = p.o32 + (head + q0) * kD;
+#pragma unroll
+        for (int dh = 0; dh < 2; ++dh)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int d0 = dh * 32 + g * 8 + hh * 4;
+                *reinterpret_cast<float4 *>(orow + d0) =
+                    make_float4(acc_o[dh][g * 4 + 0] * inv, acc_o[dh][g * 4 + 1] * inv,
+                                acc_o[dh][g * 4 + 2] * inv, acc_o[dh][g * 4 + 3] * inv);
+            }
+    } else if (q0 < N) {
         uint16_t *orow = p.o + (head + q0) * kD;
 #pragma unroll
         for (int dh = 0; dh < 2; ++dh)

@@ -160,7 +160,7 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
 
 static int attn_common(const ress_shape *shape, const void *q, const void *k, const void *v,
                        const int32_t *kept_count, const int32_t *kept_idx, float scale, void *o,
-                       bool sparse, hipStream_t stream)
+                       bool sparse, bool out_f32, hipStream_t stream)
 {
     Grid g;
     int st = check_shape(shape, &g);
@@ -184,7 +184,8 @@ static int attn_common(const ress_shape *shape, const void *q, const void *k, co
     ap.q = static_cast<const uint16_t *>(q);
     ap.k = static_cast<const uint16_t *>(k);
     ap.v = static_cast<const uint16_t *>(v);
-    ap.o = static_cast<uint16_t *>(o);
+    ap.o = out_f32 ? nullptr : static_cast<uint16_t *>(o);
+    ap.o32 = out_f32 ? static_cast<float *>(o) : nullptr;
     ap.kept_count = kept_count;
     ap.kept_idx = kept_idx;
     if (ress::launch_attn(ap, shape->bq, shape->bk, sparse, stream) != hipSuccess) return RESS_E_HIP;
@@ -195,13 +196,20 @@ int ress_sparse_attn(const ress_shape *shape, const void *q, const void *k, cons
                      const int32_t *kept_count, const int32_t *kept_idx, float scale, void *o,
                      hipStream_t stream)
 {
-    return attn_common(shape, q, k, v, kept_count, kept_idx, scale, o, true, stream);
+    return attn_common(shape, q, k, v, kept_count, kept_idx, scale, o, true, false, stream);
+}
+
+int ress_sparse_attn_out_f32(const ress_shape *shape, const void *q, const void *k, const void *v,
+                             const int32_t *kept_count, const int32_t *kept_idx, float scale, float *o,
+                             hipStream_t stream)
+{
+    return attn_common(shape, q, k, v, kept_count, kept_idx, scale, o, true, true, stream);
 }
 
 int ress_dense_attn(const ress_shape *shape, const void *q, const void *k, const void *v, float scale,
                     void *o, hipStream_t stream)
 {
-    return attn_common(shape, q, k, v, nullptr, nullptr, scale, o, false, stream);
+    return attn_common(shape, q, k, v, nullptr, nullptr, scale, o, false, false, stream);
 }
 
 }  // extern "C"

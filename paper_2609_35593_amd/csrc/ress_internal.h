@@ -49,7 +49,8 @@ struct AttnParams {
     int items_per_xcd;  // work items assigned to each of the 8 XCDs
     float scale_log2;   // softmax scale * log2(e)
     const uint16_t *q, *k, *v;
-    uint16_t *o;
+    uint16_t *o;                           // bf16 output, unless o32 is set
+    float *o32;                            // float32 output (null: write o)
     const int32_t *kept_count, *kept_idx;  // null for dense attention
 };
 

@@ -14,7 +14,7 @@ HEADER = os.path.join(ROOT, "include", "ress.h")
 def declared_entry_points():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(ress_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(ress_[a-z0-9_]+)\s*\(", src)))
 
 
 @pytest.fixture(scope="module")
@@ -26,7 +26,7 @@ def ress():
 
 def test_header_declares_the_boundary():
     assert declared_entry_points() == ["ress_dense_attn", "ress_select", "ress_select_workspace_size",
-                                       "ress_sparse_attn", "ress_status_string"]
+                                       "ress_sparse_attn", "ress_sparse_attn_out_f32", "ress_status_string"]
 
 
 def test_library_exports_every_declared_symbol(ress):
@@ -117,6 +117,11 @@ def test_attention_rejects_before_launch(ress):
                                     None) == ress.RESS_E_INVALID_ARG  # o aliases q
     assert ress.lib.ress_sparse_attn(C.byref(shape), p, C.c_void_p(1 << 43), C.c_void_p(1 << 44), None, p,
                                      0.125, o, None) == ress.RESS_E_INVALID_ARG
+    for fn in (ress.lib.ress_sparse_attn, ress.lib.ress_sparse_attn_out_f32):
+        assert fn(C.byref(shape), p, C.c_void_p(1 << 43), C.c_void_p(1 << 44), p, p, 0.125, p,
+                  None) == ress.RESS_E_INVALID_ARG  # o aliases q
+        assert fn(C.byref(shape), p, C.c_void_p(1 << 43), C.c_void_p(1 << 44), p, p, 0.125,
+                  C.c_void_p((1 << 42) + 4), None) == ress.RESS_E_INVALID_ARG  # o not 16-byte aligned
     for misaligned in ((p, C.c_void_p((1 << 43) + 2), C.c_void_p(1 << 44), o),
                        (p, C.c_void_p(1 << 43), C.c_void_p(1 << 44), C.c_void_p((1 << 42) + 8))):
         assert ress.lib.ress_dense_attn(C.byref(shape), misaligned[0], misaligned[1], misaligned[2], 0.125,

@@ -176,6 +176,30 @@ def test_attention_logit_ranges(ress):
     torch.cuda.synchronize()
     compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label="logit ranges sparse")
 
+
+def test_block_masking_change(ress):
+    """Sec. 2's single-block masking reference through ress_sparse_attn_out_f32
+    against the oracle, for rows of every head (first, middle, special tail),
+    every key block; and the Spearman correlations it feeds."""
+    import oracle
+    from paper_2609_35593_amd import masking
+
+    L = small("b128")
+    say(f"[masking reference] H={L.H} N={L.N} n_kb={L.n_kb}")
+    q, k, v, gram = device_inputs(L)
+    got = masking.block_masking_change(q, k, v, gram, bq=L.bq, bk=L.bk)
+    sel, _ = gpu_select(L, (q, k, v, gram))
+    worst = 0.0
+    for h, i in ((0, 0), (1, L.n_qb // 2), (2, 7), (3, L.n_qb - 1)):
+        ref = oracle.block_masking_change(L.q, L.k, L.v, L.gram, N=L.N, bq=L.bq, bk=L.bk, scale=1 / math.sqrt(64),
+                                          h=h, i=i, blocks=list(range(L.n_kb)))
+        rel = np.abs(got[h, i] - ref) / np.maximum(ref, 1e-2 * ref.max())
+        worst = max(worst, float(rel.max()))
+        assert rel.max() <= 2e-2, (h, i, float(rel.max()))
+        p = sel["prob"][h, i]
+        assert abs(masking.spearman_rows(got[h, i], p) - oracle.spearman(ref, p)) <= 2e-2
+    say(f"  masking change: worst relative error {worst:.2e}")
+
 # ------------------------------------------------------------------ the five workloads
 
 
