@@ -88,6 +88,8 @@ typedef struct {
     int dense_special_queries; /* nonzero: query blocks holding special tokens keep every key block */
     int criterion;             /* RESS_CRITERION_*, 0..3 */
     double cdf_tau;            /* CDF threshold in [0, 1]; 0 = off; nonzero only with PROBABILITY */
+    int pooled_in_workspace;   /* nonzero: step 1 was done by ress_qkv_proj_pool into this
+                                  workspace; q, k, v are then not read (may be NULL) */
 } ress_select_params;
 
 /* Bytes of device workspace ress_select needs for `shape` (pooled tensors,
@@ -162,6 +164,39 @@ int ress_sparse_attn_out_f32(const ress_shape *shape, const void *q, const void 
  * (the baseline the paper compares against, Table S6). */
 int ress_dense_attn(const ress_shape *shape, const void *q, const void *k, const void *v,
                     float scale, void *o, hipStream_t stream);
+
+/* The step before the path, fused: the QKV projection of one layer,
+ *   [Q K V]_t = W_qkv x_t   (x_t the layer-normed residual-stream token),
+ * written head-major, with the block mean pooling of Sec. 3 step (1) (and
+ * U_j = M_h Vbar_j, Eq. 9) taken from the bf16 outputs in the projection's
+ * epilogue, so that ress_select with params->pooled_in_workspace set does not
+ * read Q, K, V from memory again. bf16 MFMA products, float32 accumulation,
+ * outputs rounded to bf16 once; pooled means in float64 over those outputs
+ * (identical to what ress_select would pool from them).
+ *   x          device bf16 [N][H*64], token-major
+ *   w_qkv      device bf16 [3*H*64][H*64], out features x in features: rows
+ *              64h .. 64h+63 give head h of Q, then H*64 rows of K, then V
+ *   q, k, v    device bf16 [H][N][64] out
+ *   gram       device float32 [H][64][64] (M_h, as for ress_select)
+ *   workspace  as for ress_select (>= ress_select_workspace_size bytes, 256-byte
+ *              aligned); receives the pooled state
+ * H must be a multiple of 4 (tiles of 256 features); N <= 2^24. Pointers 16-byte
+ * aligned; outputs must not alias inputs. */
+int ress_qkv_proj_pool(const ress_shape *shape, const void *x, const void *w_qkv, void *q, void *k, void *v,
+                       const float *gram, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* The step after the path, fused: output projection and residual add,
+ *   resid_out_t = resid_in_t + W_O concat_h(O[h][t])
+ * reading the head-major attention output directly. bf16 MFMA products, float32
+ * accumulation, the residual added in float32 and the sum rounded to bf16 once.
+ *   o          device bf16 [H][N][64] (ress_sparse_attn's output)
+ *   w_o        device bf16 [H*64][H*64], out features x in features (in = 64h + d)
+ *   resid_in   device bf16 [N][H*64]
+ *   resid_out  device bf16 [N][H*64] out; may be resid_in (in place), must not
+ *              alias o or w_o
+ * H must be a multiple of 4. Pointers 16-byte aligned. */
+int ress_out_proj_residual(const ress_shape *shape, const void *o, const void *w_o, const void *resid_in,
+                           void *resid_out, hipStream_t stream);
 
 /* Human-readable name of a status code (static string). */
 const char *ress_status_string(int status);

@@ -277,3 +277,35 @@ def spearman(a, b) -> float:
     rb -= rb.mean()
     den = np.sqrt(np.dot(ra, ra) * np.dot(rb, rb))
     return float(np.dot(ra, rb) / den) if den > 0 else float("nan")
+
+
+def bf16_bits_nearest(x) -> np.ndarray:
+    """float64 values rounded once to the nearest bf16 (ties to even), as uint16
+    bit patterns (finite values in the normal range)."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)                       # x = m 2^e, 0.5 <= |m| < 1
+    r = np.ldexp(np.round(np.ldexp(m, 8)), e - 8)  # 8 significant bits, np.round: half to even
+    return (r.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def _f64(bits) -> np.ndarray:
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def qkv_projection(x, w_qkv, H: int):
+    """The layer's QKV projection, [Q K V]_t = W_qkv x_t, from bf16 bits x [N][64H]
+    and w_qkv [3*64H][64H], in float64, each output rounded once to bf16; returns
+    the bits of q, k, v [H][N][64] (rows 64h .. 64h+63 of each third are head h)."""
+    y = _f64(x) @ _f64(w_qkv).T              # [N][3*64H]
+    N = y.shape[0]
+    parts = y.reshape(N, 3, H, 64).transpose(1, 2, 0, 3)  # [3][H][N][64]
+    b = bf16_bits_nearest(parts)
+    return b[0], b[1], b[2]
+
+
+def out_projection_residual(o, w_o, resid):
+    """resid_t + W_O concat_h(O[h][t]) in float64 from bf16 bits o [H][N][64],
+    w_o [64H][64H], resid [N][64H], rounded once to bf16 (bits [N][64H])."""
+    H, N, D = np.asarray(o).shape
+    flat = _f64(o).transpose(1, 0, 2).reshape(N, H * D)
+    return bf16_bits_nearest(_f64(resid) + flat @ _f64(w_o).T)

@@ -33,7 +33,8 @@ class ress_shape(C.Structure):
 
 class ress_select_params(C.Structure):
     _fields_ = [("rounds", C.c_int), ("rho", C.c_double), ("eps", C.c_double), ("swap_floor", C.c_int),
-                ("dense_special_queries", C.c_int), ("criterion", C.c_int), ("cdf_tau", C.c_double)]
+                ("dense_special_queries", C.c_int), ("criterion", C.c_int), ("cdf_tau", C.c_double),
+                ("pooled_in_workspace", C.c_int)]
 
 
 # Selection criteria (include/ress.h).
@@ -64,6 +65,10 @@ def _load():
     L.ress_sparse_attn_out_f32.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, f, vp, vp]
     L.ress_sparse_attn_out_f32.restype = i
     L.ress_dense_attn.argtypes = [C.POINTER(ress_shape), vp, vp, vp, f, vp, vp]
+    L.ress_qkv_proj_pool.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.ress_qkv_proj_pool.restype = i
+    L.ress_out_proj_residual.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp]
+    L.ress_out_proj_residual.restype = i
     L.ress_dense_attn.restype = i
     return L
 
@@ -114,9 +119,12 @@ def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail:
                 rounds: int = 5, rho: float = 0.5, eps: float = 1e-4, swap_floor: int = 1,
                 dense_special_queries: bool = True, criterion: int = CRITERION_DRIFT, cdf_tau: float = 0.0,
                 kept_count=None, kept_idx=None, drift=None, key_out=None, prob_out=None,
-                want_drift: bool = True, want_debug: bool = False, workspace=None, stream=None) -> dict:
+                want_drift: bool = True, want_debug: bool = False, workspace=None,
+                pooled_in_workspace: bool = False, stream=None) -> dict:
     """Drift-based block selection for one layer (see include/ress.h).
-    keep_budget: host int32 [H]. Returns the output tensors in a dict."""
+    keep_budget: host int32 [H]. With pooled_in_workspace, `workspace` holds the
+    pooled state written by ress_qkv_proj_pool (q, k, v give the shape only).
+    Returns the output tensors in a dict."""
     _check_qkv(q, k, v)
     H, N, D = q.shape
     shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
@@ -142,7 +150,7 @@ def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail:
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     params = ress_select_params(int(rounds), float(rho), float(eps), int(swap_floor), int(bool(dense_special_queries)),
-                                int(criterion), float(cdf_tau))
+                                int(criterion), float(cdf_tau), int(bool(pooled_in_workspace)))
     st = lib.ress_select(C.byref(shape), C.byref(params), _ptr(q), _ptr(k), _ptr(v), _ptr(gram),
                          budget.ctypes.data, _ptr(kept_count), _ptr(kept_idx), _ptr(drift), _ptr(key_out),
                          _ptr(prob_out), _ptr(workspace), workspace.numel(), _stream(stream, dev))
@@ -201,6 +209,57 @@ def ress_dense_attn(q, k, v, *, bq: int, bk: int, n_special_tail: int = 0, scale
     if st != RESS_OK:
         raise RessError(st, "ress_dense_attn")
     return out
+
+
+def _check_bf16(name, t, shape):
+    if not (t.is_cuda and t.dtype == torch.bfloat16 and t.is_contiguous() and tuple(t.shape) == tuple(shape)):
+        raise ValueError(f"{name} must be a contiguous CUDA bfloat16 tensor of shape {tuple(shape)}")
+
+
+def ress_qkv_proj_pool(x, w_qkv, gram, *, bq: int, bk: int, n_special_tail: int = 0, q=None, k=None, v=None,
+                       workspace=None, stream=None) -> dict:
+    """QKV projection with block pooling in its epilogue (see include/ress.h).
+    x: bf16 [N][H*64]; w_qkv: bf16 [3*H*64][H*64]. Returns q, k, v (bf16
+    [H][N][64]) and the workspace holding the pooled state, for ress_select(...,
+    workspace=..., pooled_in_workspace=True)."""
+    N, dm = x.shape
+    H, D = dm // 64, 64
+    _check_bf16("x", x, (N, dm))
+    _check_bf16("w_qkv", w_qkv, (3 * dm, dm))
+    if not (gram.is_cuda and gram.dtype == torch.float32 and gram.is_contiguous() and gram.shape == (H, D, D)):
+        raise ValueError("gram must be a contiguous CUDA float32 tensor [H][D][D]")
+    dev = x.device
+    shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
+    q = torch.empty((H, N, D), dtype=torch.bfloat16, device=dev) if q is None else q
+    k = torch.empty((H, N, D), dtype=torch.bfloat16, device=dev) if k is None else k
+    v = torch.empty((H, N, D), dtype=torch.bfloat16, device=dev) if v is None else v
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_bf16(name, t, (H, N, D))
+    need = ress_select_workspace_size(shape)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = lib.ress_qkv_proj_pool(C.byref(shape), _ptr(x), _ptr(w_qkv), _ptr(q), _ptr(k), _ptr(v), _ptr(gram),
+                                _ptr(workspace), workspace.numel(), _stream(stream, dev))
+    if st != RESS_OK:
+        raise RessError(st, "ress_qkv_proj_pool")
+    return dict(q=q, k=k, v=v, workspace=workspace)
+
+
+def ress_out_proj_residual(o, w_o, resid_in, *, resid_out=None, stream=None):
+    """resid_out = resid_in + concat_h(o[h]) w_o^T (see include/ress.h).
+    o: bf16 [H][N][64]; w_o: bf16 [H*64][H*64]; resid_in/out: bf16 [N][H*64]."""
+    H, N, D = o.shape
+    _check_bf16("o", o, (H, N, D))
+    _check_bf16("w_o", w_o, (H * D, H * D))
+    _check_bf16("resid_in", resid_in, (N, H * D))
+    resid_out = torch.empty_like(resid_in) if resid_out is None else resid_out
+    _check_bf16("resid_out", resid_out, (N, H * D))
+    shape = make_shape(H, N, bq=128, bk=128, D=D)
+    st = lib.ress_out_proj_residual(C.byref(shape), _ptr(o), _ptr(w_o), _ptr(resid_in), _ptr(resid_out),
+                                    _stream(stream, o.device))
+    if st != RESS_OK:
+        raise RessError(st, "ress_out_proj_residual")
+    return resid_out
 
 
 def bf16_from_bits(bits: np.ndarray, device) -> torch.Tensor:

@@ -40,6 +40,21 @@ size_t workspace_bytes(const ress_shape *s, const Grid &g)
     return qb + 4 * kb;
 }
 
+// Pooled state inside the workspace (the regions workspace_bytes sizes).
+ress::Pooled pooled_layout(const ress_shape *s, const Grid &g, void *workspace)
+{
+    char *w = static_cast<char *>(workspace);
+    const size_t qb = align256((size_t)s->H * g.n_qb * kD * sizeof(double));
+    const size_t kb = align256((size_t)s->H * g.n_kb * kD * sizeof(double));
+    ress::Pooled pooled;
+    pooled.qbar = reinterpret_cast<double *>(w);
+    pooled.kbarT = reinterpret_cast<double *>(w + qb);
+    pooled.vbar = reinterpret_cast<double *>(w + qb + kb);
+    pooled.vbarT = reinterpret_cast<double *>(w + qb + 2 * kb);
+    pooled.uT = reinterpret_cast<double *>(w + qb + 3 * kb);
+    return pooled;
+}
+
 int first_forced_block(const ress_shape *s, const Grid &g)
 {
     return s->n_special_tail > 0 ? (s->N - s->n_special_tail) / s->bk : (int)g.n_kb;
@@ -90,8 +105,10 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
         (params->cdf_tau > 0.0 && params->criterion != RESS_CRITERION_PROBABILITY))
         return RESS_E_INVALID_ARG;
     if (!has_work(shape)) return RESS_OK;
-    if (!q || !k || !v || !gram || !keep_budget || !kept_count || !kept_idx) return RESS_E_INVALID_ARG;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return RESS_E_INVALID_ARG;
+    const bool pooled_ready = params->pooled_in_workspace != 0;
+    if (!gram || !keep_budget || !kept_count || !kept_idx) return RESS_E_INVALID_ARG;
+    if (!pooled_ready && (!q || !k || !v || !aligned16(q) || !aligned16(k) || !aligned16(v)))
+        return RESS_E_INVALID_ARG;
 
     const int n_kb = (int)g.n_kb, n_qb = (int)g.n_qb;
     const int first_forced = first_forced_block(shape, g);
@@ -104,17 +121,7 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
     const size_t need = workspace_bytes(shape, g);
     if (!workspace || ws_bytes < need || ((uintptr_t)workspace & 255u)) return RESS_E_WORKSPACE;
 
-    ress::Pooled pooled;
-    {
-        char *w = static_cast<char *>(workspace);
-        const size_t qb = align256((size_t)shape->H * n_qb * kD * sizeof(double));
-        const size_t kb = align256((size_t)shape->H * n_kb * kD * sizeof(double));
-        pooled.qbar = reinterpret_cast<double *>(w);
-        pooled.kbarT = reinterpret_cast<double *>(w + qb);
-        pooled.vbar = reinterpret_cast<double *>(w + qb + kb);
-        pooled.vbarT = reinterpret_cast<double *>(w + qb + 2 * kb);
-        pooled.uT = reinterpret_cast<double *>(w + qb + 3 * kb);
-    }
+    const ress::Pooled pooled = pooled_layout(shape, g, workspace);
 
     ress::PoolParams pp;
     pp.H = shape->H;
@@ -153,8 +160,83 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
     sp.prob_out = prob_out;
     for (int h = 0; h < shape->H; ++h) sp.budgets[h] = keep_budget[h];
 
-    if (ress::launch_pool(pp, stream) != hipSuccess) return RESS_E_HIP;
+    if (!pooled_ready && ress::launch_pool(pp, stream) != hipSuccess) return RESS_E_HIP;
     if (ress::launch_select(sp, stream) != hipSuccess) return RESS_E_HIP;
+    return RESS_OK;
+}
+
+// Shared checks of the two projections: shape, H a multiple of 4, grid size.
+static int proj_common(const ress_shape *shape, Grid *g, ress::ProjParams *pp, int n_out_per_head)
+{
+    int st = check_shape(shape, g);
+    if (st != RESS_OK) return st;
+    if (shape->H % 4 != 0) return RESS_E_UNSUPPORTED;
+    memset(pp, 0, sizeof *pp);
+    pp->T = shape->N;
+    pp->H = shape->H;
+    pp->m_tiles = (shape->N + 255) / 256;
+    pp->n_tiles = n_out_per_head * shape->H / 256;
+    const long long items = (long long)pp->m_tiles * pp->n_tiles;
+    const long long per_xcd = (items + 7) / 8;
+    if (8 * per_xcd > 0x7fffffffLL) return RESS_E_UNSUPPORTED;
+    pp->items_per_xcd = (int)per_xcd;
+    return RESS_OK;
+}
+
+int ress_qkv_proj_pool(const ress_shape *shape, const void *x, const void *w_qkv, void *q, void *k, void *v,
+                       const float *gram, void *workspace, size_t ws_bytes, hipStream_t stream)
+{
+    Grid g;
+    ress::ProjParams pp;
+    int st = proj_common(shape, &g, &pp, 3 * kD);
+    if (st != RESS_OK) return st;
+    if (g.n_kb > RESS_MAX_KEY_BLOCKS) return RESS_E_UNSUPPORTED;
+    if (!has_work(shape)) return RESS_OK;
+    if (!x || !w_qkv || !q || !k || !v || !gram) return RESS_E_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(w_qkv) || !aligned16(q) || !aligned16(k) || !aligned16(v))
+        return RESS_E_INVALID_ARG;
+    const void *ins[2] = {x, w_qkv};
+    void *outs[3] = {q, k, v};
+    for (void *o : outs)
+        for (const void *in : ins)
+            if (o == in) return RESS_E_INVALID_ARG;
+    if (q == k || q == v || k == v) return RESS_E_INVALID_ARG;
+    const size_t need = workspace_bytes(shape, g);
+    if (!workspace || ws_bytes < need || ((uintptr_t)workspace & 255u)) return RESS_E_WORKSPACE;
+    pp.mode = 0;
+    pp.bq = shape->bq;
+    pp.bk = shape->bk;
+    pp.n_qb = (int)g.n_qb;
+    pp.n_kb = (int)g.n_kb;
+    pp.a = static_cast<const uint16_t *>(x);
+    pp.w = static_cast<const uint16_t *>(w_qkv);
+    pp.q = static_cast<uint16_t *>(q);
+    pp.k = static_cast<uint16_t *>(k);
+    pp.v = static_cast<uint16_t *>(v);
+    pp.gram = gram;
+    pp.pooled = pooled_layout(shape, g, workspace);
+    if (ress::launch_proj(pp, stream) != hipSuccess) return RESS_E_HIP;
+    return RESS_OK;
+}
+
+int ress_out_proj_residual(const ress_shape *shape, const void *o, const void *w_o, const void *resid_in,
+                           void *resid_out, hipStream_t stream)
+{
+    Grid g;
+    ress::ProjParams pp;
+    int st = proj_common(shape, &g, &pp, kD);
+    if (st != RESS_OK) return st;
+    if (!has_work(shape)) return RESS_OK;
+    if (!o || !w_o || !resid_in || !resid_out) return RESS_E_INVALID_ARG;
+    if (!aligned16(o) || !aligned16(w_o) || !aligned16(resid_in) || !aligned16(resid_out))
+        return RESS_E_INVALID_ARG;
+    if (resid_out == o || resid_out == w_o) return RESS_E_INVALID_ARG;
+    pp.mode = 1;
+    pp.a = static_cast<const uint16_t *>(o);
+    pp.w = static_cast<const uint16_t *>(w_o);
+    pp.resid_in = static_cast<const uint16_t *>(resid_in);
+    pp.resid_out = static_cast<uint16_t *>(resid_out);
+    if (ress::launch_proj(pp, stream) != hipSuccess) return RESS_E_HIP;
     return RESS_OK;
 }
 

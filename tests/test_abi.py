@@ -5,6 +5,7 @@ import ctypes as C
 import os
 import re
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -25,8 +26,9 @@ def ress():
 
 
 def test_header_declares_the_boundary():
-    assert declared_entry_points() == ["ress_dense_attn", "ress_select", "ress_select_workspace_size",
-                                       "ress_sparse_attn", "ress_sparse_attn_out_f32", "ress_status_string"]
+    assert declared_entry_points() == ["ress_dense_attn", "ress_out_proj_residual", "ress_qkv_proj_pool",
+                                       "ress_select", "ress_select_workspace_size", "ress_sparse_attn",
+                                       "ress_sparse_attn_out_f32", "ress_status_string"]
 
 
 def test_library_exports_every_declared_symbol(ress):
@@ -132,3 +134,46 @@ def test_attention_rejects_before_launch(ress):
     assert ress.lib.ress_dense_attn(C.byref(bad), p, p, p, 0.125, o, None) == ress.RESS_E_UNSUPPORTED
     empty = ress.make_shape(2, 0, bq=64, bk=64)
     assert ress.lib.ress_dense_attn(C.byref(empty), None, None, None, 0.125, None, None) == ress.RESS_OK
+
+
+def test_projections_reject_before_launch(ress):
+    """Validation of the fused projections (nothing is launched on these paths)."""
+    p = [C.c_void_p((1 << 41) + (n << 30)) for n in range(6)]
+    ws = C.c_void_p(1 << 40)
+    shape = ress.make_shape(8, 1000, bq=128, bk=128)
+    need = ress.ress_select_workspace_size(shape)
+    qkv = ress.lib.ress_qkv_proj_pool
+    assert qkv(C.byref(ress.make_shape(6, 1000, bq=128, bk=128)), p[0], p[1], p[2], p[3], p[4], p[5], ws, need,
+               None) == ress.RESS_E_UNSUPPORTED  # H not a multiple of 4
+    assert qkv(C.byref(shape), p[0], p[1], p[2], p[3], p[4], p[5], ws, need - 1, None) == ress.RESS_E_WORKSPACE
+    assert qkv(C.byref(shape), p[0], p[1], p[2], p[3], p[4], p[5], C.c_void_p((1 << 40) + 64), need,
+               None) == ress.RESS_E_WORKSPACE  # not 256-byte aligned
+    assert qkv(C.byref(shape), p[0], p[1], p[0], p[3], p[4], p[5], ws, need, None) == ress.RESS_E_INVALID_ARG
+    assert qkv(C.byref(shape), p[0], p[1], p[2], p[2], p[4], p[5], ws, need, None) == ress.RESS_E_INVALID_ARG
+    assert qkv(C.byref(shape), p[0], None, p[2], p[3], p[4], p[5], ws, need, None) == ress.RESS_E_INVALID_ARG
+    assert qkv(C.byref(shape), C.c_void_p((1 << 41) + 8), p[1], p[2], p[3], p[4], p[5], ws, need,
+               None) == ress.RESS_E_INVALID_ARG  # x not 16-byte aligned
+    empty = ress.make_shape(8, 0, bq=128, bk=128)
+    assert qkv(C.byref(empty), None, None, None, None, None, None, None, 0, None) == ress.RESS_OK
+    out = ress.lib.ress_out_proj_residual
+    assert out(C.byref(ress.make_shape(2, 1000, bq=128, bk=128)), p[0], p[1], p[2], p[3],
+               None) == ress.RESS_E_UNSUPPORTED
+    assert out(C.byref(shape), p[0], p[1], p[2], p[0], None) == ress.RESS_E_INVALID_ARG  # resid_out aliases o
+    assert out(C.byref(shape), p[0], p[1], p[2], None, None) == ress.RESS_E_INVALID_ARG
+    assert out(C.byref(empty), None, None, None, None, None) == ress.RESS_OK
+
+
+def test_select_with_pooled_state_needs_no_qkv(ress):
+    """pooled_in_workspace: q, k, v may be NULL; everything else is still checked."""
+    shape = ress.make_shape(2, 1230, bq=64, bk=64)
+    params = ress.ress_select_params(5, 0.5, 1e-4, 1, 1, 0, 0.0, 1)
+    budget = np.array([6, 6], np.int32)
+    need = ress.ress_select_workspace_size(shape)
+    p = C.c_void_p(1 << 41)
+    st = ress.lib.ress_select(C.byref(shape), C.byref(params), None, None, None, p, budget.ctypes.data, p, p, None,
+                              None, None, C.c_void_p(1 << 40), need - 1, None)
+    assert st == ress.RESS_E_WORKSPACE  # reached the workspace check: q, k, v were not required
+    params.pooled_in_workspace = 0
+    st = ress.lib.ress_select(C.byref(shape), C.byref(params), None, None, None, p, budget.ctypes.data, p, p, None,
+                              None, None, C.c_void_p(1 << 40), need, None)
+    assert st == ress.RESS_E_INVALID_ARG
