@@ -45,6 +45,7 @@ def parse():
     ap.add_argument("--no-flush", action="store_true", help="skip the cache-flushed secondary timing")
     ap.add_argument("--no-criteria", action="store_true", help="skip the per-criterion drift report")
     ap.add_argument("--no-masking", action="store_true", help="skip the single-block masking report")
+    ap.add_argument("--no-neighbours", action="store_true", help="skip the fused-projection report")
     ap.add_argument("--rounds", type=int, default=5)
     ap.add_argument("--dense-steps", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
@@ -226,6 +227,74 @@ def masking_report(ress, L, q, k, v, gram, stream):
     return out
 
 
+def neighbours_report(ress, L, stream, reps=10):
+    """The steps on either side of the path at this layer's shape, fused into our
+    GEMMs against the vendor GEMM (hipBLASLt through torch) plus the layout copies
+    and the separate pooling pass the unfused chain needs. Inputs are random
+    (x ~ N(0, 1), weights ~ N(0, 1/width)); every time is the mean of `reps`
+    back-to-back launches between HIP events on the library's stream."""
+    import torch
+
+    dev = torch.device("cuda:0")
+    H, N = L.H, L.N
+    dm = 64 * H
+    g = torch.Generator(device=dev).manual_seed(7)
+    x = torch.randn(N, dm, device=dev, generator=g).bfloat16()
+    w_qkv = (torch.randn(3 * dm, dm, device=dev, generator=g) / dm ** 0.5).bfloat16()
+    w_o = (torch.randn(dm, dm, device=dev, generator=g) / dm ** 0.5).bfloat16()
+    resid = torch.randn(N, dm, device=dev, generator=g).bfloat16()
+    o = torch.randn(H, N, 64, device=dev, generator=g).bfloat16()
+    gram = torch.from_numpy(L.gram).to(dev)
+    fused = ress.ress_qkv_proj_pool(x, w_qkv, gram, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail, stream=stream)
+    q, k, v, ws = fused["q"], fused["k"], fused["v"], fused["workspace"]
+    y = torch.empty(N, 3 * dm, device=dev, dtype=torch.bfloat16)
+    r_out = torch.empty_like(resid)
+    sel_kw = dict(bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail, stream=stream)
+
+    def timed(fn):
+        with torch.cuda.stream(stream):
+            fn()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(reps):
+                fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    def vendor_qkv():
+        torch.mm(x, w_qkv.t(), out=y)
+        yy = y.view(N, 3, H, 64).permute(1, 2, 0, 3)
+        q.copy_(yy[0])
+        k.copy_(yy[1])
+        v.copy_(yy[2])
+
+    def vendor_out():
+        torch.addmm(resid, o.permute(1, 0, 2).reshape(N, dm), w_o.t(), out=r_out)
+
+    t_qkv = timed(lambda: ress.ress_qkv_proj_pool(x, w_qkv, gram, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                                                  q=q, k=k, v=v, workspace=ws, stream=stream))
+    t_sel_pooled = timed(lambda: ress.ress_select(q, k, v, gram, L.budgets, workspace=ws, pooled_in_workspace=True,
+                                                  **sel_kw))
+    t_sel_plain = timed(lambda: ress.ress_select(q, k, v, gram, L.budgets, **sel_kw))
+    t_mm = timed(lambda: torch.mm(x, w_qkv.t(), out=y))
+    t_vqkv = timed(vendor_qkv)
+    t_out = timed(lambda: ress.ress_out_proj_residual(o, w_o, resid, resid_out=r_out, stream=stream))
+    t_vout = timed(vendor_out)
+    fl_qkv, fl_out = 2.0 * N * dm * 3 * dm, 2.0 * N * dm * dm
+    tf = lambda fl, ms: round(fl / (ms * 1e-3) / 1e12, 1)
+    return {
+        "qkv_proj_pool_ms": round(t_qkv, 4), "qkv_proj_pool_tflops": tf(fl_qkv, t_qkv),
+        "vendor_qkv_mm_ms": round(t_mm, 4), "vendor_qkv_mm_tflops": tf(fl_qkv, t_mm),
+        "vendor_qkv_mm_plus_head_major_ms": round(t_vqkv, 4),
+        "select_from_fused_pooling_ms": round(t_sel_pooled, 4), "select_with_own_pooling_ms": round(t_sel_plain, 4),
+        "before_path_fused_ms": round(t_qkv + t_sel_pooled, 4),
+        "before_path_unfused_ms": round(t_vqkv + t_sel_plain, 4),
+        "out_proj_residual_ms": round(t_out, 4), "out_proj_residual_tflops": tf(fl_out, t_out),
+        "vendor_permute_addmm_ms": round(t_vout, 4), "vendor_permute_addmm_tflops": tf(fl_out, t_vout),
+    }
+
+
 def copy_calibration():
     import torch
 
@@ -333,6 +402,7 @@ def main():
     ceilings = measured_ceilings(torch, dev)
     criteria = None if args.no_criteria else criteria_report(ress, L, q, k, v, gram, od, stream)
     mask_rep = None if args.no_masking else masking_report(ress, L, q, k, v, gram, stream)
+    neigh = None if args.no_neighbours else neighbours_report(ress, L, stream)
 
     kc_h, ki_h, dr = kc.cpu().numpy(), ki.cpu().numpy(), drift.cpu().numpy().reshape(-1, 2)
     flops_kept, kept_tiles = kept_flops(L, kc_h, ki_h)
@@ -403,6 +473,7 @@ def main():
             "cache_flushed": flushed,
             "criteria_same_budget": criteria,
             "single_block_masking": mask_rep,
+            "fused_neighbours": neigh,
             "input_generation_s": round(gen_s, 1),
         },
     }
