@@ -110,28 +110,42 @@ __global__ void __launch_bounds__(kThreads, 1) proj_kernel(const ProjParams p)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
 
+    // Operand fragments are read one k-step (16) ahead into two register sets, so
+    // the LDS latency of step kk+1 hides behind the 8 MFMAs of step kk; the first
+    // step of the next k-tile is read right after the barrier, beside the MFMAs of
+    // the last step of this one.
+    bf16x8 fa[2][2], fb[2][4];
+    auto read_frags = [&](int slot, int kk, int buf) __attribute__((always_inline)) {
+        const unsigned char *A = slot_ptr(slot, 0), *B = slot_ptr(slot, 1);
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi) fa[buf][mi] = *reinterpret_cast<const bf16x8 *>(A + aoff[mi][kk]);
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) fb[buf][ni] = *reinterpret_cast<const bf16x8 *>(B + boff[ni][kk]);
+    };
+    auto mfmas = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 4; ++ni)
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][mi], fb[buf][ni], acc[mi][ni], 0, 0, 0);
+    };
+
     dma(0, 0);
     wait_vm_all();
     __syncthreads();
+    read_frags(0, 0, 0);
     for (int kt = 0; kt < KT; ++kt) {
         const int slot = kt & 1;
         if (kt + 1 < KT) dma(kt + 1, slot ^ 1);
-        const unsigned char *A = slot_ptr(slot, 0), *B = slot_ptr(slot, 1);
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            bf16x8 a[2], b[4];
-#pragma unroll
-            for (int mi = 0; mi < 2; ++mi) a[mi] = *reinterpret_cast<const bf16x8 *>(A + aoff[mi][kk]);
-#pragma unroll
-            for (int ni = 0; ni < 4; ++ni) b[ni] = *reinterpret_cast<const bf16x8 *>(B + boff[ni][kk]);
-#pragma unroll
-            for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-                for (int ni = 0; ni < 4; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
+        for (int kk = 0; kk < 3; ++kk) {
+            read_frags(slot, kk + 1, (kk + 1) & 1);
+            mfmas(kk & 1);
         }
         wait_vm_all();    // k-tile kt + 1 has landed (this wave's part) ...
         __syncthreads();  // ... every wave's, and slot kt & 1 is no longer read
+        if (kt + 1 < KT) read_frags(slot ^ 1, 0, 0);
+        mfmas(1);         // step 3 of this k-tile
     }
 
     // Accumulator element (mi, ni, v) of this lane: tile row and column.
