@@ -168,7 +168,7 @@ int ress_dense_attn(const ress_shape *shape, const void *q, const void *k, const
 /* The step before the path, fused: the QKV projection of one layer,
  *   [Q K V]_t = W_qkv x_t   (x_t the layer-normed residual-stream token),
  * written head-major, with the block mean pooling of Sec. 3 step (1) (and
- * U_j = M_h Vbar_j, Eq. 9) taken from the bf16 outputs in the projection's
+ * Vbar_j^T M_h Vbar_j, Eq. 9) taken from the bf16 outputs in the projection's
  * epilogue, so that ress_select with params->pooled_in_workspace set does not
  * read Q, K, V from memory again. bf16 MFMA products, float32 accumulation,
  * outputs rounded to bf16 once; pooled means in float64 over those outputs

@@ -1,5 +1,5 @@
 // Block mean pooling of Q, K and V (the coarse block grid of Sec. 3, step (1)),
-// plus U_j = M_h Vbar_j for the drift scores (Eq. 9).
+// plus c_j = Vbar_j^T M_h Vbar_j for the drift scores (Eq. 9).
 //
 // One wave per pooled block; a workgroup holds 4 waves that pool 4 consecutive
 // blocks of the same head and tensor, so the channel-major outputs are written
@@ -19,6 +19,14 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;  // blocks per workgroup
+
+// Sum over the wave by a fixed butterfly (commutative adds: identical in every lane).
+__device__ __forceinline__ double wave_sum(double x)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+    return x;
+}
 
 __device__ __forceinline__ void accum_bf16x8(double (&acc)[8], uint4 w)
 {
@@ -61,7 +69,7 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
 {
     __shared__ float Ms[kD * (kD + 1)];       // M_h, padded rows (V workgroups)
     __shared__ double vb[kWaves][kD];         // each wave's Vbar_j
-    __shared__ double tile[2][kD][kWaves];    // channel-major outputs of the 4 blocks
+    __shared__ double tile[kD][kWaves];       // channel-major outputs of the 4 blocks
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
     const int gq = (p.n_qb + kWaves - 1) / kWaves, gk = (p.n_kb + kWaves - 1) / kWaves;
@@ -93,7 +101,7 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
             p.out.vbar[((size_t)h * p.n_kb + j) * kD + lane] = mean;
             vb[wave][lane] = mean;
         }
-        tile[0][lane][wave] = mean;
+        tile[lane][wave] = mean;
     }
     if (is_v) {  // M_h row r, column c at r * 65 + c
 #pragma unroll
@@ -107,22 +115,17 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
         }
     }
     __syncthreads();
-    if (is_v && j < p.n_kb) {  // U_j = M_h Vbar_j, lane t <-> output channel t
+    if (is_v && j < p.n_kb) {  // c_j = sum_t Vbar_jt (M_h Vbar_j)_t
         double u = 0.0;
         for (int c = 0; c < kD; ++c) u = fma((double)Ms[lane * (kD + 1) + c], vb[wave][c], u);
-        tile[1][lane][wave] = u;
+        const double cj = wave_sum(u * vb[wave][lane]);
+        if (lane == 0) p.out.cT[(size_t)h * p.n_kb + j] = cj;
     }
-    __syncthreads();
     // Channel-major outputs: thread (row, w) writes block j0 + w of channel row.
     const int row = t >> 2, w = t & 3;
     if (w < nb) {
         const size_t off = ((size_t)h * kD + row) * p.n_kb + j0 + w;
-        if (is_v) {
-            p.out.vbarT[off] = tile[0][row][w];
-            p.out.uT[off] = tile[1][row][w];
-        } else {
-            p.out.kbarT[off] = tile[0][row][w];
-        }
+        (is_v ? p.out.vbarT : p.out.kbarT)[off] = tile[row][w];
     }
 }
 

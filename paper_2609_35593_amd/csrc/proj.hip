@@ -2,7 +2,7 @@
 // epilogues (token-major activations, nn.Linear-style [out][in] weights):
 //  - QKV projection, [Q K V] = X W_qkv^T, written head-major [H][N][64], with the
 //    block mean pooling of Sec. 3 step (1) taken from the bf16-rounded outputs in
-//    the epilogue (plus U_j = M_h Vbar_j for Eq. 9), so the selection never reads
+//    the epilogue (plus c_j = Vbar_j^T M_h Vbar_j for Eq. 9), so the selection never reads
 //    Q, K, V again;
 //  - output projection and residual add, R' = R + concat_h(O_h) W_O^T, reading
 //    the head-major attention output directly (the k-slice of one 64-wide k-tile
@@ -230,7 +230,8 @@ __global__ void __launch_bounds__(kThreads, 1) proj_kernel(const ProjParams p)
             }
         }
         if (which == 2) {
-            // U_j = M_h Vbar_j: one wave per (block, head) of the tile, lane <-> channel.
+            // c_j = Vbar_j . (M_h Vbar_j): one wave per (block, head) of the tile, lane <->
+            // channel, in the same order as the pooling pass of the selection.
             __syncthreads();
             const int nblk = BM / b, pairs = nblk * (BN / 64);
             for (int pr = wave; pr < pairs; pr += kThreads / 64) {
@@ -243,7 +244,10 @@ __global__ void __launch_bounds__(kThreads, 1) proj_kernel(const ProjParams p)
                 double u = 0.0;
 #pragma unroll 8
                 for (int c = 0; c < 64; ++c) u = fma((double)Mrow[c], vb[c], u);
-                p.pooled.uT[((size_t)h * 64 + lane) * p.n_kb + t0 / b] = u;
+                double cj = u * vb[lane];
+#pragma unroll
+                for (int o = 32; o >= 1; o >>= 1) cj += __shfl_xor(cj, o);
+                if (lane == 0) p.pooled.cT[(size_t)h * p.n_kb + t0 / b] = cj;
             }
         }
     } else {

@@ -31,13 +31,14 @@ bool has_work(const ress_shape *s) { return s->H > 0 && s->N > 0; }
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 bool aligned16(const void *ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 
-// Workspace: qbar [H][n_qb][64], then kbarT, vbar, vbarT, uT, each [H][n_kb][64]
-// (float64), every region 256-byte aligned.
+// Workspace: qbar [H][n_qb][64], then kbarT, vbar, vbarT, each [H][n_kb][64], then
+// cT [H][n_kb] (float64), every region 256-byte aligned.
 size_t workspace_bytes(const ress_shape *s, const Grid &g)
 {
     const size_t qb = align256((size_t)s->H * g.n_qb * kD * sizeof(double));
     const size_t kb = align256((size_t)s->H * g.n_kb * kD * sizeof(double));
-    return qb + 4 * kb;
+    const size_t cb = align256((size_t)s->H * g.n_kb * sizeof(double));
+    return qb + 3 * kb + cb;
 }
 
 // Pooled state inside the workspace (the regions workspace_bytes sizes).
@@ -51,7 +52,7 @@ ress::Pooled pooled_layout(const ress_shape *s, const Grid &g, void *workspace)
     pooled.kbarT = reinterpret_cast<double *>(w + qb);
     pooled.vbar = reinterpret_cast<double *>(w + qb + kb);
     pooled.vbarT = reinterpret_cast<double *>(w + qb + 2 * kb);
-    pooled.uT = reinterpret_cast<double *>(w + qb + 3 * kb);
+    pooled.cT = reinterpret_cast<double *>(w + qb + 3 * kb);
     return pooled;
 }
 

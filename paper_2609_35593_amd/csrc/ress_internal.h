@@ -18,7 +18,7 @@ struct Pooled {
     double *kbarT;  // [H][64][n_kb]   key block means, channel-major
     double *vbar;   // [H][n_kb][64]   value block means
     double *vbarT;  // [H][64][n_kb]   value block means, channel-major
-    double *uT;     // [H][64][n_kb]   M_h Vbar_j, channel-major
+    double *cT;     // [H][n_kb]       Vbar_j^T M_h Vbar_j
 };
 
 struct PoolParams {

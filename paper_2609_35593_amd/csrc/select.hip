@@ -117,14 +117,20 @@ struct WaveLds {
 
 // x_r = M_h y_r for the R rows (lane <-> channel), M row-major in LDS (padded
 // rows), y_r broadcast from LDS two channels at a time.
-template <int R>
+// x_r = M y_r, lane <-> output channel; with SYM, x_r = (M + M^T)/2 y_r (the matrix
+// whose quadratic form equals that of M, exact in float64 from float32 entries).
+template <int R, bool SYM>
 __device__ __forceinline__ void mat_vec(const float *Ms, double *const (&y)[R], double (&x)[R], int lane)
 {
 #pragma unroll
     for (int r = 0; r < R; ++r) x[r] = 0.0;
 #pragma unroll 4
     for (int b = 0; b < kD; b += 2) {
-        const double m0 = (double)Ms[lane * (kD + 1) + b], m1 = (double)Ms[lane * (kD + 1) + b + 1];
+        double m0 = (double)Ms[lane * (kD + 1) + b], m1 = (double)Ms[lane * (kD + 1) + b + 1];
+        if (SYM) {
+            m0 = 0.5 * (m0 + (double)Ms[b * (kD + 1) + lane]);
+            m1 = 0.5 * (m1 + (double)Ms[(b + 1) * (kD + 1) + lane]);
+        }
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const double2 yb = *reinterpret_cast<const double2 *>(y[r] + b);
@@ -209,7 +215,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
     const double *Kt = p.pooled.kbarT + (size_t)h * kD * nkb;
     const double *Vr = p.pooled.vbar + (size_t)h * nkb * kD;
     const double *Vt = p.pooled.vbarT + (size_t)h * kD * nkb;
-    const double *Ut = p.pooled.uT + (size_t)h * kD * nkb;
+    const double *cT = p.pooled.cT + (size_t)h * nkb;
     const int c_h = p.budgets[h];
     const int n_p = p.first_forced;  // candidates are the key blocks j < first_forced
 
@@ -282,35 +288,41 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
         }
     }
 
-    // Dense pooled output vbar_i = sum_j P_ij Vbar_j and M vbar_i (lane <-> channel).
+    // Dense pooled output vbar_i = sum_j P_ij Vbar_j, w_i = S vbar_i with S the
+    // symmetric part of M (lane <-> channel), and vbar_i^T S vbar_i.
+    double vsv[R];
     {
         double vb[R], wv[R];
         block_pass<CPL, R, false>(lds, P, vb, Vr, nkb, lane, vb);
 #pragma unroll
         for (int r = 0; r < R; ++r) vbv[r][lane] = vb[r];
         __builtin_amdgcn_wave_barrier();
-        mat_vec<R>(Ms, vbv, wv, lane);
+        mat_vec<R, true>(Ms, vbv, wv, lane);
 #pragma unroll
-        for (int r = 0; r < R; ++r) wvv[r][lane] = wv[r];
+        for (int r = 0; r < R; ++r) {
+            wvv[r][lane] = wv[r];
+            vsv[r] = wave_sum(vb[r] * wv[r]);
+        }
         __builtin_amdgcn_wave_barrier();
     }
 
-    // q_ij = e^T M e with e = vbar_i - Vbar_j, as e . (M vbar_i - M Vbar_j) (Eq. 9);
-    // s_ij = P_ij sqrt(q_ij), key_ij = s_ij / max(1 - P_ij, eps) (Eqs. 6-7).
+    // q_ij = e^T M e with e = vbar_i - Vbar_j (Eq. 9), expanded through the symmetric
+    // part S of M (same quadratic form): q = vbar_i^T S vbar_i - 2 Vbar_j . w_i +
+    // Vbar_j^T M Vbar_j, the last term per block from the pooling pass; one column of
+    // Vbar per candidate. s_ij = P_ij sqrt(q_ij), key_ij = s_ij / max(1 - P_ij, eps)
+    // (Eqs. 6-7).
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
-        const double *vcol = Vt + jc[c], *ucol = Ut + jc[c];
+        const double *vcol = Vt + jc[c];
 #pragma unroll
         for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
 #pragma unroll kUnroll<CPL>
         for (int d = 0; d < kD; d += 2) {
             const double v0 = vcol[(size_t)d * nkb], v1 = vcol[(size_t)(d + 1) * nkb];
-            const double u0 = ucol[(size_t)d * nkb], u1 = ucol[(size_t)(d + 1) * nkb];
 #pragma unroll
             for (int r = 0; r < R; ++r) {
-                const double2 vb = *reinterpret_cast<const double2 *>(vbv[r] + d);
                 const double2 wd = *reinterpret_cast<const double2 *>(wvv[r] + d);
-                acc[r][c] = fma(vb.y - v1, wd.y - u1, fma(vb.x - v0, wd.x - u0, acc[r][c]));
+                acc[r][c] = fma(v1, wd.y, fma(v0, wd.x, acc[r][c]));
             }
         }
     }
@@ -318,7 +330,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
     for (int r = 0; r < R; ++r) {
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-            const double q = acc[r][c];
+            const double q = fma(-2.0, acc[r][c], vsv[r] + cT[jc[c]]);
             const double s = P[r][c] * sqrt(q > 0.0 ? q : 0.0);
             const double den = 1.0 - P[r][c];
             S2[r][c] = s * s;
@@ -413,7 +425,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
     auto objective = [&]() {  // h = M g, G = g . h, J = G / max(K, eps)^2
         __builtin_amdgcn_wave_barrier();
         double hh[R];
-        mat_vec<R>(Ms, gv, hh, lane);
+        mat_vec<R, false>(Ms, gv, hh, lane);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             hv[r][lane] = hh[r];
