@@ -181,6 +181,8 @@ def test_block_masking_change(ress):
     """Sec. 2's single-block masking reference through ress_sparse_attn_out_f32
     against the oracle, for rows of every head (first, middle, special tail),
     every key block; and the Spearman correlations it feeds."""
+    import torch
+
     import oracle
     from paper_2609_35593_amd import masking
 
@@ -199,6 +201,12 @@ def test_block_masking_change(ress):
         p = sel["prob"][h, i]
         assert abs(masking.spearman_rows(got[h, i], p) - oracle.spearman(ref, p)) <= 2e-2
     say(f"  masking change: worst relative error {worst:.2e}")
+    # The float32 output is the bf16 output before its final rounding.
+    kc, ki = torch.from_numpy(sel["kept_count"]).cuda(), torch.from_numpy(sel["kept_idx"]).cuda()
+    o16 = ress.ress_sparse_attn(q, k, v, kc, ki, bq=L.bq, bk=L.bk)
+    o32 = ress.ress_sparse_attn_out_f32(q, k, v, kc, ki, bq=L.bq, bk=L.bk)
+    torch.cuda.synchronize()
+    assert torch.equal(o32.bfloat16(), o16)
 
 # ------------------------------------------------------------------ the five workloads
 

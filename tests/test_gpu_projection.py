@@ -65,7 +65,8 @@ def _qkv_bounds(x, w_qkv, H):
     return parts[0], parts[1], parts[2]
 
 
-CASES = [(4, 1000, 128, 128, 11), (4, 777, 64, 128, 12), (16, 2755, 128, 64, 13)]
+CASES = [(4, 1000, 128, 128, 11), (4, 777, 64, 128, 12), (16, 2755, 128, 64, 13), (4, 1, 64, 64, 15),
+         (8, 130, 128, 64, 16)]
 
 
 @pytest.mark.parametrize("H,N,bq,bk,seed", CASES)
@@ -84,7 +85,7 @@ def test_qkv_projection_and_pooled_selection(ress, H, N, bq, bk, seed):
         _check(got, r, bnd, f"{name} H={H} N={N}")
     # The pooled state from the epilogue against ress_select pooling the same q, k, v.
     n_kb = (N + bk - 1) // bk
-    budgets = np.full(H, max(2, n_kb // 3), np.int32)
+    budgets = np.full(H, min(n_kb, max(2, n_kb // 3)), np.int32)
     q, k, v = out["q"], out["k"], out["v"]
     fused = ress.ress_select(q, k, v, gram_d, budgets, bq=bq, bk=bk, want_debug=True, workspace=out["workspace"],
                              pooled_in_workspace=True)
