@@ -188,6 +188,65 @@ constexpr int kMinBlocks = (CPL == 6 && R == 2) ? 3 : 1;
 template <int CPL>
 constexpr int kUnroll = CPL >= 17 ? 2 : 4;
 
+// acc[r][c] = sum_d T[d][jc[c]] * x_r[d] over the 64 channels of a channel-major
+// pooled tensor T (lane <-> key block), in ascending d with the same fused
+// multiply-adds whichever loop order is used. SUB: sum_d (y_r[d] - T[d][jc[c]]) x_r[d].
+// Few slots and rows: channels outermost, so the loads of every slot are in flight
+// together; otherwise slots outermost (fewer registers held by loads; measured:
+// the channel-outer order costs the 4-slot, 4-row shape its second wave per SIMD).
+template <int CPL, int R, bool SUB>
+__device__ __forceinline__ void column_dots(const double *__restrict__ T, const int (&jc)[CPL], int nkb,
+                                            double *const (&x)[R], double *const (&y)[R], double (&acc)[R][CPL])
+{
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
+    if constexpr (CPL <= 8 && CPL * R <= 12) {
+#pragma unroll 1
+        for (int d = 0; d < kD; d += 2) {
+            double t0[CPL], t1[CPL];
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                t0[c] = T[(size_t)d * nkb + jc[c]];
+                t1[c] = T[(size_t)(d + 1) * nkb + jc[c]];
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const double2 xd = *reinterpret_cast<const double2 *>(x[r] + d);
+                double2 yd = {0.0, 0.0};
+                if (SUB) yd = *reinterpret_cast<const double2 *>(y[r] + d);
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    if (SUB)
+                        acc[r][c] = fma(yd.y - t1[c], xd.y, fma(yd.x - t0[c], xd.x, acc[r][c]));
+                    else
+                        acc[r][c] = fma(xd.y, t1[c], fma(xd.x, t0[c], acc[r][c]));
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const double *col = T + jc[c];
+#pragma unroll kUnroll<CPL>
+            for (int d = 0; d < kD; d += 2) {
+                const double t0 = col[(size_t)d * nkb], t1 = col[(size_t)(d + 1) * nkb];
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const double2 xd = *reinterpret_cast<const double2 *>(x[r] + d);
+                    if (SUB) {
+                        const double2 yd = *reinterpret_cast<const double2 *>(y[r] + d);
+                        acc[r][c] = fma(yd.y - t1, xd.y, fma(yd.x - t0, xd.x, acc[r][c]));
+                    } else {
+                        acc[r][c] = fma(xd.y, t1, fma(xd.x, t0, acc[r][c]));
+                    }
+                }
+            }
+        }
+    }
+}
+
 template <int CPL, int R, bool CDF>
 __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(const SelectParams p)
 {
@@ -246,20 +305,9 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
 
     // Pooled logits Qbar_i . Kbar_j / sqrt(D) (Eq. 1).
     double acc[R][CPL], P[R][CPL], S2[R][CPL];
+    column_dots<CPL, R, false>(Kt, jc, nkb, vbv, vbv, acc);
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
-        const double *col = Kt + jc[c];
-#pragma unroll
-        for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
-#pragma unroll kUnroll<CPL>
-        for (int d = 0; d < kD; d += 2) {
-            const double k0 = col[(size_t)d * nkb], k1 = col[(size_t)(d + 1) * nkb];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const double2 qd = *reinterpret_cast<const double2 *>(vbv[r] + d);
-                acc[r][c] = fma(qd.y, k1, fma(qd.x, k0, acc[r][c]));
-            }
-        }
     }
     // Softmax over all key blocks.
 #pragma unroll
@@ -311,21 +359,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
     // Vbar_j^T M Vbar_j, the last term per block from the pooling pass; one column of
     // Vbar per candidate. s_ij = P_ij sqrt(q_ij), key_ij = s_ij / max(1 - P_ij, eps)
     // (Eqs. 6-7).
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-        const double *vcol = Vt + jc[c];
-#pragma unroll
-        for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
-#pragma unroll kUnroll<CPL>
-        for (int d = 0; d < kD; d += 2) {
-            const double v0 = vcol[(size_t)d * nkb], v1 = vcol[(size_t)(d + 1) * nkb];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const double2 wd = *reinterpret_cast<const double2 *>(wvv[r] + d);
-                acc[r][c] = fma(v1, wd.y, fma(v0, wd.x, acc[r][c]));
-            }
-        }
-    }
+    column_dots<CPL, R, false>(Vt, jc, nkb, wvv, wvv, acc);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
 #pragma unroll
@@ -456,22 +490,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
         }
         if (mmax <= 0) break;
         // e_k . (M g) for every candidate k of every row.
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            const double *vcol = Vt + jc[c];
-#pragma unroll
-            for (int r = 0; r < R; ++r) acc[r][c] = 0.0;
-#pragma unroll kUnroll<CPL>
-            for (int d = 0; d < kD; d += 2) {
-                const double v0 = vcol[(size_t)d * nkb], v1 = vcol[(size_t)(d + 1) * nkb];
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const double2 vb = *reinterpret_cast<const double2 *>(vbv[r] + d);
-                    const double2 hd = *reinterpret_cast<const double2 *>(hv[r] + d);
-                    acc[r][c] = fma(vb.y - v1, hd.y, fma(vb.x - v0, hd.x, acc[r][c]));
-                }
-            }
-        }
+        column_dots<CPL, R, true>(Vt, jc, nkb, hv, vbv, acc);
         // Gains of every single restore / drop at the round-start state; the m best
         // of each kind are applied together, g and K following Eq. 13.
 #pragma unroll
