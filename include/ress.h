@@ -2,11 +2,14 @@
  * ress.h - C ABI of the MI355X (gfx950) hot path of ReSS, "Residual-Restoring
  * Sparse Attention for 3D Vision Transformers": drift-based block selection
  * followed by block-sparse attention over the kept blocks, plus the dense
- * attention it is measured against.
+ * attention it is measured against, and the projections on either side of the
+ * path (QKV projection with the pooling fused in, output projection with the
+ * residual add).
  *
  * Conventions shared by every entry point
  *  - Tensors Q, K, V, O are bf16, laid out [H][N][D] contiguous (head-major, then
- *    token, then channel), one layer of batch 1, with D == 64.
+ *    token, then channel), one layer of batch 1, with D == 64. The projections'
+ *    activations and weights are token-major / [out][in], as documented there.
  *  - Tokens are grouped into fixed-size blocks: query block i covers tokens
  *    [i*bq, min((i+1)*bq, N)), key block j covers [j*bk, min((j+1)*bk, N))
  *    (the paper's block grid, Sec. 3 step (1)); the last block of each kind may be
@@ -139,7 +142,11 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
  * i attends exactly to the tokens of the key blocks kept_idx[h][i][0 ..
  * kept_count[h][i]-1], with the softmax renormalised among them:
  *   O_t = sum_s softmax_s(scale * Q_t . K_s) V_s.
- * bf16 MFMA products, float32 softmax and accumulation.
+ * bf16 MFMA products, float32 softmax and accumulation, probabilities rounded to
+ * bf16 for the PV product. For a 32-row group of queries whose first 64 logits
+ * lie within +-24 (base 2), Q is multiplied by scale * log2(e) and rounded to
+ * bf16 before the products (one extra relative rounding of 2^-9 per element of
+ * Q); other groups use Q as given.
  *   kept_count  device int32 [H][n_qb]; values are clamped to [0, n_kb]
  *   kept_idx    device int32 [H][n_qb][n_kb]; entries outside [0, n_kb) are
  *               ignored (contribute no keys); duplicates count twice

@@ -7,7 +7,8 @@
 // tensors is used by the R rows in registers and by the 4 waves through L1.
 //  - Per-candidate quantities live "lane <-> key block": lane l, slot c holds key
 //    block j = l + 64 c (CPL slots).
-//  - Per-row vectors (Qbar, vbar, M vbar, g, M g) live "lane <-> channel"
+//  - Per-row vectors (Qbar, vbar, S vbar with S the symmetric part of M, g, M g)
+//    live "lane <-> channel"
 //    (D = 64 is the wave width) and are broadcast to the candidate lanes through
 //    the wave's LDS area, two doubles per read.
 //  - Every top-k is exact: a bitwise search for the k-th largest of
