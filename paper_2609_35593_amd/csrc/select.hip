@@ -116,10 +116,10 @@ struct WaveLds {
     __device__ int *swap_j() const { return reinterpret_cast<int *>(base + kVecs * R * kD + R * 64 + 64); }
 };
 
-// x_r = M_h y_r for the R rows (lane <-> channel), M row-major in LDS (padded
-// rows), y_r broadcast from LDS two channels at a time.
-// x_r = M y_r, lane <-> output channel; with SYM, x_r = (M + M^T)/2 y_r (the matrix
-// whose quadratic form equals that of M, exact in float64 from float32 entries).
+// x_r = M y_r for the R rows, lane <-> output channel, M row-major in LDS (padded
+// rows), y_r broadcast from LDS two channels at a time; with SYM, x_r = (M + M^T)/2
+// y_r (the matrix whose quadratic form equals that of M, exact in float64 from
+// float32 entries).
 template <int R, bool SYM>
 __device__ __forceinline__ void mat_vec(const float *Ms, double *const (&y)[R], double (&x)[R], int lane)
 {
@@ -517,34 +517,43 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
             double mr = 0.0, md = 0.0;
             double g = gv[r][lane];
             const double vbl = vbv[r][lane];
+            // The swapped blocks of all slots, in slot order, are gathered into one list
+            // (up to 64 entries) and applied 8 rows of Vbar at a time: restores
+            // subtract d_k, drops add it (zero weights pad the last group exactly).
+            int nbuf = 0;
+            auto apply = [&]() __attribute__((always_inline)) {
+                __builtin_amdgcn_wave_barrier();
+                for (int t0 = 0; t0 < nbuf; t0 += 8) {
+                    double vj[8], wj[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int t = min(t0 + u, nbuf - 1);
+                        vj[u] = Vr[(size_t)swap_j[t] * kD + lane];
+                        wj[u] = t0 + u < nbuf ? swap_w[t] : 0.0;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) g = fma(wj[u], vbl - vj[u], g);
+                }
+                __builtin_amdgcn_wave_barrier();
+                nbuf = 0;
+            };
 #pragma unroll
             for (int c = 0; c < CPL; ++c) {
-                // Compact this slot's swapped blocks: restores subtract d_k, drops add it.
                 const bool is_rest = (rest >> c) & 1ull, is_drop = (drop >> c) & 1ull;
                 const unsigned long long sm = __ballot(is_rest || is_drop);
                 if (sm == 0ull) continue;
-                __builtin_amdgcn_wave_barrier();
+                const int n = __popcll(sm);
+                if (nbuf + n > 64) apply();
                 if (is_rest || is_drop) {
-                    const int pos = __popcll(sm & lane_lt);
+                    const int pos = nbuf + __popcll(sm & lane_lt);
                     swap_j[pos] = lane + 64 * c;
                     swap_w[pos] = is_drop ? P[r][c] : -P[r][c];
                 }
                 if (is_rest) mr += P[r][c];
                 if (is_drop) md += P[r][c];
-                __builtin_amdgcn_wave_barrier();
-                const int n = __popcll(sm);
-                for (int t0 = 0; t0 < n; t0 += 8) {
-                    double vj[8], wj[8];
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) {
-                        const int t = min(t0 + u, n - 1);
-                        vj[u] = Vr[(size_t)swap_j[t] * kD + lane];
-                        wj[u] = t0 + u < n ? swap_w[t] : 0.0;
-                    }
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) g = fma(wj[u], vbl - vj[u], g);
-                }
+                nbuf += n;
             }
+            if (nbuf > 0) apply();
             K[r] = (K[r] + wave_sum(mr)) - wave_sum(md);
             __builtin_amdgcn_wave_barrier();
             gv[r][lane] = g;
