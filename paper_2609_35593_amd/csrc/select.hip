@@ -26,6 +26,24 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+// Word 3 of a raw buffer descriptor on gfx9-family chips (32-bit data format,
+// no swizzle, no index stride): loads past num_records bytes return zero.
+constexpr int kBufWord3 = 0x00020000;
+
+// Buffer descriptor over one head's pooled tensor (n_kb x 64 doubles, either layout).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t pooled_rsrc(const double *base, int nkb)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<double *>(base), 0, kD * nkb * (int)sizeof(double),
+                                             kBufWord3);
+}
+
+// Channel `lane` of row j (wave-uniform) of a row-major pooled tensor.
+__device__ __forceinline__ double pooled_row(__amdgpu_buffer_rsrc_t rs, int j, int lane)
+{
+    return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(
+                                          rs, (unsigned)lane * (unsigned)sizeof(double),
+                                          __builtin_amdgcn_readfirstlane(j) * kD * (int)sizeof(double), 0));
+}
 
 __device__ __forceinline__ double wave_sum(double x)
 {
@@ -104,16 +122,19 @@ __device__ __forceinline__ int swaps_of_round(int c, double rho, int r, int swap
 }
 
 // Per-wave LDS area (doubles): broadcast vectors vec[slot][R][64], one slot of
-// block weights wts[R][64], and a swap list of up to 64 (block, weight) pairs.
+// block weights wts[R][64], and a swap list of up to 64 (block, weight) pairs plus
+// padding to a multiple of 8. Every part starts on a 16-byte boundary.
 template <int R>
 struct WaveLds {
     static constexpr int kVecs = 3;  // 0: Qbar then vbar, 1: M vbar then M g, 2: g
-    static constexpr int kDoubles = kVecs * R * kD + R * 64 + 64 + 32;
+    static constexpr int kSwaps = 72;
+    static constexpr int kDoubles = kVecs * R * kD + R * 64 + kSwaps + kSwaps / 2;
+    static_assert(kDoubles % 2 == 0, "16-byte aligned wave areas");
     double *base;
     __device__ double *vec(int slot, int r) const { return base + (slot * R + r) * kD; }
     __device__ double *wts(int r) const { return base + kVecs * R * kD + r * 64; }
     __device__ double *swap_w() const { return base + kVecs * R * kD + R * 64; }
-    __device__ int *swap_j() const { return reinterpret_cast<int *>(base + kVecs * R * kD + R * 64 + 64); }
+    __device__ int *swap_j() const { return reinterpret_cast<int *>(base + kVecs * R * kD + R * 64 + kSwaps); }
 };
 
 // x_r = M y_r for the R rows, lane <-> output channel, M row-major in LDS (padded
@@ -150,6 +171,7 @@ template <int CPL, int R, bool SUB>
 __device__ __forceinline__ void block_pass(const WaveLds<R> &lds, const double (&w)[R][CPL], const double (&x)[R],
                                            const double *__restrict__ Vr, int nkb, int lane, double (&out)[R])
 {
+    const __amdgpu_buffer_rsrc_t rsV = pooled_rsrc(Vr, nkb);
 #pragma unroll
     for (int r = 0; r < R; ++r) out[r] = 0.0;
 #pragma unroll
@@ -159,11 +181,10 @@ __device__ __forceinline__ void block_pass(const WaveLds<R> &lds, const double (
         for (int r = 0; r < R; ++r) lds.wts(r)[lane] = w[r][c];  // 0 past the last block
         __builtin_amdgcn_wave_barrier();
         const int lim = min(64, nkb - 64 * c);
-        const double *vrow = Vr + (size_t)64 * c * kD;
         for (int l0 = 0; l0 < lim; l0 += 8) {
             double vj[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) vj[u] = vrow[(size_t)min(l0 + u, lim - 1) * kD + lane];
+            for (int u = 0; u < 8; ++u) vj[u] = pooled_row(rsV, 64 * c + min(l0 + u, lim - 1), lane);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const double *wr = lds.wts(r) + l0;
@@ -203,14 +224,24 @@ __device__ __forceinline__ void column_dots(const double *__restrict__ T, const 
     for (int r = 0; r < R; ++r)
 #pragma unroll
         for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
+    // Buffer loads: a per-lane 32-bit byte offset (the key block) and a wave-uniform
+    // one (the channel row), range-checked by the hardware against the head's tensor.
+    const __amdgpu_buffer_rsrc_t rs = pooled_rsrc(T, nkb);
+    unsigned off[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) off[c] = (unsigned)jc[c] * (unsigned)sizeof(double);
+    const int stride = nkb * (int)sizeof(double);
+    auto at = [&](int d, int c) __attribute__((always_inline)) {
+        return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(rs, off[c], d * stride, 0));
+    };
     if constexpr (CPL <= 8 && CPL * R <= 12) {
 #pragma unroll 1
         for (int d = 0; d < kD; d += 2) {
             double t0[CPL], t1[CPL];
 #pragma unroll
             for (int c = 0; c < CPL; ++c) {
-                t0[c] = T[(size_t)d * nkb + jc[c]];
-                t1[c] = T[(size_t)(d + 1) * nkb + jc[c]];
+                t0[c] = at(d, c);
+                t1[c] = at(d + 1, c);
             }
 #pragma unroll
             for (int r = 0; r < R; ++r) {
@@ -229,10 +260,9 @@ __device__ __forceinline__ void column_dots(const double *__restrict__ T, const 
     } else {
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-            const double *col = T + jc[c];
 #pragma unroll kUnroll<CPL>
             for (int d = 0; d < kD; d += 2) {
-                const double t0 = col[(size_t)d * nkb], t1 = col[(size_t)(d + 1) * nkb];
+                const double t0 = at(d, c), t1 = at(d + 1, c);
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const double2 xd = *reinterpret_cast<const double2 *>(x[r] + d);
@@ -251,7 +281,7 @@ __device__ __forceinline__ void column_dots(const double *__restrict__ T, const 
 template <int CPL, int R, bool CDF>
 __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(const SelectParams p)
 {
-    __shared__ double smem[kWaves * WaveLds<R>::kDoubles];
+    __shared__ __align__(16) double smem[kWaves * WaveLds<R>::kDoubles];
     __shared__ float Ms[kD * (kD + 1)];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const unsigned long long lane_bit = 1ull << lane, lane_lt = lane_bit - 1ull;
@@ -479,6 +509,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
 
     // Budget-neutral restoration rounds (Eqs. 13-17) with track-best. The swap
     // count follows each row's kept count; rows whose count reached 0 are done.
+    const __amdgpu_buffer_rsrc_t rsV = pooled_rsrc(Vr, nkb);
     double *swap_w = lds.swap_w();
     int *swap_j = lds.swap_j();
     for (int rr = 0; rr < p.rounds; ++rr) {
@@ -519,20 +550,30 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
             const double vbl = vbv[r][lane];
             // The swapped blocks of all slots, in slot order, are gathered into one list
             // (up to 64 entries) and applied 8 rows of Vbar at a time: restores
-            // subtract d_k, drops add it (zero weights pad the last group exactly).
+            // subtract d_k, drops add it. The list is padded to a multiple of 8 with
+            // zero-weight entries of block 0, which leave g unchanged.
             int nbuf = 0;
             auto apply = [&]() __attribute__((always_inline)) {
+                const int nr = (nbuf + 7) & ~7;
+                if (lane < nr - nbuf) {
+                    swap_j[nbuf + lane] = 0;
+                    swap_w[nbuf + lane] = 0.0;
+                }
                 __builtin_amdgcn_wave_barrier();
-                for (int t0 = 0; t0 < nbuf; t0 += 8) {
-                    double vj[8], wj[8];
+                for (int t0 = 0; t0 < nr; t0 += 8) {
+                    const int4 ja = *reinterpret_cast<const int4 *>(swap_j + t0);
+                    const int4 jb = *reinterpret_cast<const int4 *>(swap_j + t0 + 4);
+                    const int js[8] = {ja.x, ja.y, ja.z, ja.w, jb.x, jb.y, jb.z, jb.w};
+                    double vj[8];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) {
-                        const int t = min(t0 + u, nbuf - 1);
-                        vj[u] = Vr[(size_t)swap_j[t] * kD + lane];
-                        wj[u] = t0 + u < nbuf ? swap_w[t] : 0.0;
+                    for (int u = 0; u < 8; ++u)
+                        vj[u] = pooled_row(rsV, js[u], lane);
+#pragma unroll
+                    for (int u = 0; u < 8; u += 2) {
+                        const double2 w = *reinterpret_cast<const double2 *>(swap_w + t0 + u);
+                        g = fma(w.x, vbl - vj[u], g);
+                        g = fma(w.y, vbl - vj[u + 1], g);
                     }
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) g = fma(wj[u], vbl - vj[u], g);
                 }
                 __builtin_amdgcn_wave_barrier();
                 nbuf = 0;
