@@ -337,9 +337,6 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
     // Pooled logits Qbar_i . Kbar_j / sqrt(D) (Eq. 1).
     double acc[R][CPL], P[R][CPL], S2[R][CPL];
     column_dots<CPL, R, false>(Kt, jc, nkb, vbv, vbv, acc);
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-    }
     // Softmax over all key blocks.
 #pragma unroll
     for (int r = 0; r < R; ++r) {
