@@ -643,16 +643,33 @@ hipError_t launch_cfg(const SelectParams &p, hipStream_t s)
     return hipGetLastError();
 }
 
+// Rows per wave: the most rows, up to RMAX, that still give each of the chip's
+// 256 compute units a workgroup. Measured: sharing every pooled-tensor load among
+// more rows pays only while the grid fills the chip (8 views, 86 blocks: 4 rows
+// per wave 0.20 ms, 1 row 0.12 ms; 16 views, 172 blocks: 4 rows 0.39 ms, 2 rows
+// 0.22 ms; 32 views, 344 blocks: 2 rows 0.48 ms, 1 row 0.70 ms).
+constexpr long long kCUs = 256;
+template <int CPL, int RMAX>
+hipError_t launch_rows(const SelectParams &p, hipStream_t s)
+{
+    auto workgroups = [&](int r) { return (long long)p.H * ((p.n_qb + kWaves * r - 1) / (kWaves * r)); };
+    if constexpr (RMAX >= 4)
+        if (workgroups(4) >= kCUs) return launch_cfg<CPL, 4>(p, s);
+    if constexpr (RMAX >= 2)
+        if (workgroups(2) >= kCUs) return launch_cfg<CPL, 2>(p, s);
+    return launch_cfg<CPL, 1>(p, s);
+}
+
 }  // namespace
 
 hipError_t launch_select(const SelectParams &p, hipStream_t s)
 {
     if (p.H == 0 || p.n_qb == 0) return hipSuccess;
     const int n = p.n_kb;
-    if (n <= 64) return launch_cfg<1, 4>(p, s);
-    if (n <= 128) return launch_cfg<2, 4>(p, s);
-    if (n <= 256) return launch_cfg<4, 4>(p, s);
-    if (n <= 384) return launch_cfg<6, 2>(p, s);
+    if (n <= 64) return launch_rows<1, 4>(p, s);
+    if (n <= 128) return launch_rows<2, 4>(p, s);
+    if (n <= 256) return launch_rows<4, 4>(p, s);
+    if (n <= 384) return launch_rows<6, 2>(p, s);
     if (n <= 512) return launch_cfg<8, 1>(p, s);
     if (n <= 768) return launch_cfg<12, 1>(p, s);
     if (n <= 1088) return launch_cfg<17, 1>(p, s);
