@@ -260,6 +260,42 @@ def test_select_one_row_per_wave_range(ress):
     _config_case(ress, L, 5, rows=rows, n_tokens=256, label="22v q128/k64")
 
 
+def _rows_per_wave(H, n_qb, n_kb):
+    """Rows per wave the selection launch takes: at most 4 (<= 256 key blocks), 2
+    (<= 384) or 1, and within that the most that still give each of the 256
+    compute units a workgroup of 4 waves."""
+    cap = 4 if n_kb <= 256 else 2 if n_kb <= 384 else 1
+    for r in (4, 2):
+        if r <= cap and H * -(-n_qb // (4 * r)) >= 256:
+            return r
+    return 1
+
+
+# (views, patch tokens per view, heads, slots per lane, rows per wave), 64-token blocks:
+# every launch shape of the selection up to 384 key blocks.
+LAUNCH_SHAPES = [(4, 1019, 64, 1, 4), (4, 1019, 32, 1, 2), (4, 1019, 16, 1, 1),
+                 (8, 1019, 32, 2, 4), (8, 1019, 16, 2, 2), (8, 1019, 8, 2, 1),
+                 (8, 2043, 16, 4, 4), (8, 2043, 8, 4, 2), (8, 2043, 4, 4, 1),
+                 (8, 3067, 8, 6, 2), (8, 3067, 4, 6, 1)]
+
+
+@pytest.mark.parametrize("views,ppv,H,cpl,rpw", LAUNCH_SHAPES)
+def test_select_launch_shapes(ress, views, ppv, H, cpl, rpw):
+    """Each (slots per lane, rows per wave) shape against the oracle on a row
+    sample, also with the probability rule under a CDF cap (its own build)."""
+    L = synth.make_layer(views, ppv, 5, H=H, block=64, sparsity=0.75, seed=40 + cpl * 4 + rpw,
+                         name=f"{views}v H={H}")
+    assert -(-L.n_kb // 64) == cpl and _rows_per_wave(L.H, L.n_qb, L.n_kb) == rpw
+    say(f"[select launch shape] slots {cpl}, rows per wave {rpw}: H={L.H} N={L.N} n_kb={L.n_kb}")
+    rng = np.random.default_rng(cpl * 10 + rpw)
+    rows = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 120), [0, L.n_qb - 1, L.H * L.n_qb - 1]]))
+    gpu, _ = gpu_select(L, rounds=5)
+    compare_select(L, gpu, oracle_select(L, rounds=5, rows=rows), rows=rows, label=f"{cpl}x{rpw}")
+    gpu, _ = gpu_select(L, rounds=3, criterion=1, cdf_tau=0.25)  # the cap binds on most rows here
+    compare_select(L, gpu, oracle_select(L, rounds=3, rows=rows, criterion=1, cdf_tau=0.25), rows=rows,
+                   label=f"{cpl}x{rpw} cdf", criterion=1, capped=True)
+
+
 def test_config_100v_ragged(ress):
     L = synth.make_config("100v")
     rng = np.random.default_rng(5)
