@@ -114,9 +114,10 @@ int ress_select_workspace_size(const ress_shape *shape, size_t *bytes);
  * Every top-k breaks ties by the lower block index. Scoring and restoration run
  * in float64.
  *
- *   q, k, v       device bf16 [H][N][D]
+ *   q, k, v       device bf16 [H][N][D], 16-byte aligned
  *   gram          device float32 [H][D][D], M_h row-major (computed once at load,
- *                 Eq. 8); used as given, M_h x means sum_b M[a][b] x[b]
+ *                 Eq. 8), 16-byte aligned; used as given, M_h x means
+ *                 sum_b M[a][b] x[b]
  *   keep_budget   HOST int32 [H]: c_h, kept candidate blocks per row. Must lie in
  *                 [min(n_p, max(0, 2 - n_forced)), n_p], n_p = candidates (the
  *                 paper's floor of two kept key blocks per query row, Supp. F)

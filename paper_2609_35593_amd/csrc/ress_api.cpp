@@ -107,7 +107,7 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
         return RESS_E_INVALID_ARG;
     if (!has_work(shape)) return RESS_OK;
     const bool pooled_ready = params->pooled_in_workspace != 0;
-    if (!gram || !keep_budget || !kept_count || !kept_idx) return RESS_E_INVALID_ARG;
+    if (!gram || !keep_budget || !kept_count || !kept_idx || !aligned16(gram)) return RESS_E_INVALID_ARG;
     if (!pooled_ready && (!q || !k || !v || !aligned16(q) || !aligned16(k) || !aligned16(v)))
         return RESS_E_INVALID_ARG;
 
@@ -194,7 +194,7 @@ int ress_qkv_proj_pool(const ress_shape *shape, const void *x, const void *w_qkv
     if (g.n_kb > RESS_MAX_KEY_BLOCKS) return RESS_E_UNSUPPORTED;
     if (!has_work(shape)) return RESS_OK;
     if (!x || !w_qkv || !q || !k || !v || !gram) return RESS_E_INVALID_ARG;
-    if (!aligned16(x) || !aligned16(w_qkv) || !aligned16(q) || !aligned16(k) || !aligned16(v))
+    if (!aligned16(x) || !aligned16(w_qkv) || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(gram))
         return RESS_E_INVALID_ARG;
     const void *ins[2] = {x, w_qkv};
     void *outs[3] = {q, k, v};

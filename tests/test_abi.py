@@ -71,10 +71,11 @@ def test_workspace_size(ress):
     assert ress.lib.ress_select_workspace_size(C.byref(shape), C.byref(C.c_size_t())) == ress.RESS_E_UNSUPPORTED
 
 
-def _select_status(ress, shape, params, budgets, ws_bytes=1 << 30, ws_ptr=1 << 40, ptr=1 << 41):
+def _select_status(ress, shape, params, budgets, ws_bytes=1 << 30, ws_ptr=1 << 40, ptr=1 << 41, gram_ptr=None):
     arr = (C.c_int32 * len(budgets))(*budgets)
     p = C.c_void_p(ptr)
-    return ress.lib.ress_select(C.byref(shape), C.byref(params) if params is not None else None, p, p, p, p,
+    gram = p if gram_ptr is None else C.c_void_p(gram_ptr)
+    return ress.lib.ress_select(C.byref(shape), C.byref(params) if params is not None else None, p, p, p, gram,
                                 C.cast(arr, C.c_void_p), p, p, None, None, None, C.c_void_p(ws_ptr), ws_bytes,
                                 None)
 
@@ -104,6 +105,7 @@ def test_select_rejects_before_launch(ress):
     assert _select_status(ress, one_forced, good, [0, 6]) == ress.RESS_E_INVALID_ARG
     assert _select_status(ress, shape, good, [6, 6], ptr=0) == ress.RESS_E_INVALID_ARG
     assert _select_status(ress, shape, good, [6, 6], ptr=(1 << 41) + 8) == ress.RESS_E_INVALID_ARG  # q/k/v not 16-byte aligned
+    assert _select_status(ress, shape, good, [6, 6], gram_ptr=(1 << 42) + 4) == ress.RESS_E_INVALID_ARG  # gram
     empty = ress.make_shape(0, 1230, bq=64, bk=64)
     assert _select_status(ress, empty, good, [], ptr=0, ws_ptr=0, ws_bytes=0) == ress.RESS_OK
 
@@ -154,6 +156,8 @@ def test_projections_reject_before_launch(ress):
     assert qkv(C.byref(shape), p[0], None, p[2], p[3], p[4], p[5], ws, need, None) == ress.RESS_E_INVALID_ARG
     assert qkv(C.byref(shape), C.c_void_p((1 << 41) + 8), p[1], p[2], p[3], p[4], p[5], ws, need,
                None) == ress.RESS_E_INVALID_ARG  # x not 16-byte aligned
+    assert qkv(C.byref(shape), p[0], p[1], p[2], p[3], p[4], C.c_void_p((1 << 41) + (5 << 30) + 4), ws, need,
+               None) == ress.RESS_E_INVALID_ARG  # gram not 16-byte aligned
     empty = ress.make_shape(8, 0, bq=128, bk=128)
     assert qkv(C.byref(empty), None, None, None, None, None, None, None, 0, None) == ress.RESS_OK
     out = ress.lib.ress_out_proj_residual
