@@ -107,6 +107,20 @@ def _check_qkv(q, k, v):
         raise ValueError("q, k, v must share shape and device")
 
 
+def _check_out(name, t, dtype, shape, device):
+    """A caller-provided output (or workspace) tensor must match what the kernels write."""
+    if not (t.is_cuda and t.device == device and t.dtype == dtype and t.is_contiguous()
+            and tuple(t.shape) == tuple(shape)):
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)} on {device}")
+
+
+def _workspace_bytes(workspace, device):
+    """Size in bytes of a caller's workspace tensor (the library checks it is enough)."""
+    if not (workspace.is_cuda and workspace.device == device and workspace.is_contiguous()):
+        raise ValueError(f"workspace must be a contiguous tensor on {device}")
+    return workspace.numel() * workspace.element_size()
+
+
 def ress_select_workspace_size(shape: ress_shape) -> int:
     n = C.c_size_t(0)
     st = lib.ress_select_workspace_size(C.byref(shape), C.byref(n))
@@ -130,8 +144,7 @@ def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail:
     shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
     n_qb, n_kb = (N + bq - 1) // bq, (N + bk - 1) // bk
     dev = q.device
-    if not (gram.is_cuda and gram.dtype == torch.float32 and gram.is_contiguous() and gram.shape == (H, D, D)):
-        raise ValueError("gram must be a contiguous CUDA float32 tensor [H][D][D]")
+    _check_out("gram", gram, torch.float32, (H, D, D), dev)
     budget = np.ascontiguousarray(np.asarray(keep_budget, dtype=np.int32).reshape(-1))
     if budget.shape[0] != H:
         raise ValueError("keep_budget must hold one int per head")
@@ -146,14 +159,21 @@ def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail:
             key_out = torch.empty((H, n_qb, n_kb), dtype=torch.float64, device=dev)
         if prob_out is None:
             prob_out = torch.empty((H, n_qb, n_kb), dtype=torch.float64, device=dev)
+    _check_out("kept_count", kept_count, torch.int32, (H, n_qb), dev)
+    _check_out("kept_idx", kept_idx, torch.int32, (H, n_qb, n_kb), dev)
+    for name, t, shp in (("drift", drift, (H, n_qb, 2)), ("key_out", key_out, (H, n_qb, n_kb)),
+                         ("prob_out", prob_out, (H, n_qb, n_kb))):
+        if t is not None:
+            _check_out(name, t, torch.float64, shp, dev)
     need = ress_select_workspace_size(shape)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    ws_bytes = _workspace_bytes(workspace, dev)
     params = ress_select_params(int(rounds), float(rho), float(eps), int(swap_floor), int(bool(dense_special_queries)),
                                 int(criterion), float(cdf_tau), int(bool(pooled_in_workspace)))
     st = lib.ress_select(C.byref(shape), C.byref(params), _ptr(q), _ptr(k), _ptr(v), _ptr(gram),
                          budget.ctypes.data, _ptr(kept_count), _ptr(kept_idx), _ptr(drift), _ptr(key_out),
-                         _ptr(prob_out), _ptr(workspace), workspace.numel(), _stream(stream, dev))
+                         _ptr(prob_out), _ptr(workspace), ws_bytes, _stream(stream, dev))
     if st != RESS_OK:
         raise RessError(st, "ress_select")
     return dict(kept_count=kept_count, kept_idx=kept_idx, drift=drift, key=key_out, prob=prob_out)
@@ -163,16 +183,15 @@ def _sparse_call(fn, name, q, k, v, kept_count, kept_idx, bq, bk, n_special_tail
     _check_qkv(q, k, v)
     H, N, D = q.shape
     shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
-    for t in (kept_count, kept_idx):
-        if not (t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()):
-            raise ValueError("kept_count / kept_idx must be contiguous CUDA int32 tensors")
     n_qb, n_kb = (N + bq - 1) // bq, (N + bk - 1) // bk
+    for name, t in (("kept_count", kept_count), ("kept_idx", kept_idx)):
+        if not (t.is_cuda and t.device == q.device and t.dtype == torch.int32 and t.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous int32 tensor on {q.device}")
     if kept_count.numel() != H * n_qb or kept_idx.numel() != H * n_qb * n_kb:
         raise ValueError("kept_count must be [H][n_qb] and kept_idx [H][n_qb][n_kb]")
     if out is None:
         out = torch.empty(q.shape, dtype=out_dtype, device=q.device)
-    if not (out.is_cuda and out.dtype == out_dtype and out.is_contiguous() and tuple(out.shape) == tuple(q.shape)):
-        raise ValueError(f"out must be a contiguous CUDA {out_dtype} tensor shaped like q")
+    _check_out("out", out, out_dtype, q.shape, q.device)
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     st = fn(C.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(kept_count), _ptr(kept_idx), float(scale), _ptr(out),
             _stream(stream, q.device))
@@ -203,6 +222,7 @@ def ress_dense_attn(q, k, v, *, bq: int, bk: int, n_special_tail: int = 0, scale
     shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
     if out is None:
         out = torch.empty_like(q)
+    _check_out("out", out, torch.bfloat16, q.shape, q.device)
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     st = lib.ress_dense_attn(C.byref(shape), _ptr(q), _ptr(k), _ptr(v), float(scale), _ptr(out),
                              _stream(stream, q.device))
@@ -226,20 +246,22 @@ def ress_qkv_proj_pool(x, w_qkv, gram, *, bq: int, bk: int, n_special_tail: int 
     H, D = dm // 64, 64
     _check_bf16("x", x, (N, dm))
     _check_bf16("w_qkv", w_qkv, (3 * dm, dm))
-    if not (gram.is_cuda and gram.dtype == torch.float32 and gram.is_contiguous() and gram.shape == (H, D, D)):
-        raise ValueError("gram must be a contiguous CUDA float32 tensor [H][D][D]")
     dev = x.device
+    if w_qkv.device != dev:
+        raise ValueError("x and w_qkv must share a device")
+    _check_out("gram", gram, torch.float32, (H, D, D), dev)
     shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
     q = torch.empty((H, N, D), dtype=torch.bfloat16, device=dev) if q is None else q
     k = torch.empty((H, N, D), dtype=torch.bfloat16, device=dev) if k is None else k
     v = torch.empty((H, N, D), dtype=torch.bfloat16, device=dev) if v is None else v
     for name, t in (("q", q), ("k", k), ("v", v)):
-        _check_bf16(name, t, (H, N, D))
+        _check_out(name, t, torch.bfloat16, (H, N, D), dev)
     need = ress_select_workspace_size(shape)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    ws_bytes = _workspace_bytes(workspace, dev)
     st = lib.ress_qkv_proj_pool(C.byref(shape), _ptr(x), _ptr(w_qkv), _ptr(q), _ptr(k), _ptr(v), _ptr(gram),
-                                _ptr(workspace), workspace.numel(), _stream(stream, dev))
+                                _ptr(workspace), ws_bytes, _stream(stream, dev))
     if st != RESS_OK:
         raise RessError(st, "ress_qkv_proj_pool")
     return dict(q=q, k=k, v=v, workspace=workspace)
@@ -254,6 +276,8 @@ def ress_out_proj_residual(o, w_o, resid_in, *, resid_out=None, stream=None):
     _check_bf16("resid_in", resid_in, (N, H * D))
     resid_out = torch.empty_like(resid_in) if resid_out is None else resid_out
     _check_bf16("resid_out", resid_out, (N, H * D))
+    if not (w_o.device == resid_in.device == resid_out.device == o.device):
+        raise ValueError("o, w_o, resid_in and resid_out must share a device")
     shape = make_shape(H, N, bq=128, bk=128, D=D)
     st = lib.ress_out_proj_residual(C.byref(shape), _ptr(o), _ptr(w_o), _ptr(resid_in), _ptr(resid_out),
                                     _stream(stream, o.device))

@@ -394,6 +394,33 @@ def test_errors_leave_outputs_untouched(ress):
     assert bool(torch.all(kc == 1234)) and bool(torch.all(ki == 1234))
 
 
+def test_binding_rejects_mismatched_outputs(ress):
+    """Caller-provided outputs of the wrong shape, type or layout are refused by the
+    binding before the library is called."""
+    import torch
+
+    L = small("forced64")
+    say("[binding] mismatched outputs")
+    q, k, v, gram = device_inputs(L)
+    kc = torch.zeros((L.H, L.n_qb), dtype=torch.int32, device="cuda")
+    ki = torch.zeros((L.H, L.n_qb, L.n_kb + 1), dtype=torch.int32, device="cuda")
+    sel = dict(bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail)
+    with pytest.raises(ValueError):
+        ress.ress_select(q, k, v, gram, L.budgets, kept_count=kc, kept_idx=ki[:, :, 1:], **sel)  # not contiguous
+    with pytest.raises(ValueError):
+        ress.ress_select(q, k, v, gram, L.budgets, kept_count=kc, kept_idx=ki, **sel)  # one column too many
+    with pytest.raises(ValueError):
+        ress.ress_select(q, k, v, gram, L.budgets, drift=torch.zeros((L.H, L.n_qb, 2), device="cuda"), **sel)
+    with pytest.raises(ValueError):
+        ress.ress_select(q, k, v, gram.double(), L.budgets, **sel)
+    out = ress.ress_select(q, k, v, gram, L.budgets, **sel)
+    with pytest.raises(ValueError):
+        ress.ress_sparse_attn(q, k, v, out["kept_count"], out["kept_idx"], out=torch.empty_like(q)[:, :-1], **sel)
+    with pytest.raises(ValueError):
+        ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, out=torch.empty(q.shape, device="cuda"))
+    torch.cuda.synchronize()
+
+
 def test_empty_shapes_are_no_ops(ress):
     import torch
 
