@@ -156,8 +156,8 @@ def measured_ceilings(torch, dev):
 
 
 def criteria_report(ress, L, q, k, v, gram, o_dense, stream):
-    """The paper's comparison of selection criteria at one budget (Table 3 rows and
-    the sign-flipped objective of Sec. 5.4), on this synthetic layer: for each
+    """The paper's comparison of selection criteria at one budget (Table 2 rows and
+    the sign-flipped objective of Fig. 8, Sec. 6.1), on this synthetic layer: for each
     criterion the median pooled drift J of the returned selection (over rows that
     drop blocks) and the token-level residual drift it leaves,
     sum ||W_O (O_sparse - O_dense)||^2 / sum ||W_O O_dense||^2 over every token and
@@ -187,7 +187,7 @@ def criteria_report(ress, L, q, k, v, gram, o_dense, stream):
 
 
 def masking_report(ress, L, q, k, v, gram, stream):
-    """Sec. 2's test of the probability assumption (Fig. 2) on this synthetic layer:
+    """Sec. 3's test of the probability assumption (Fig. 2) on this synthetic layer:
     mask one candidate key block at a time (every query block attends to all other
     blocks, float32 outputs from this library's kernel) and measure the change
     ||W_O (O_masked - O_dense)|| over each query block's tokens; then, per selected

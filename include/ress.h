@@ -64,12 +64,12 @@ typedef struct {
 /* Selection criteria. RESS_CRITERION_DRIFT is the method (Secs. 4.2-4.3); the
  * others are the comparisons the paper makes with the same budget:
  *   PROBABILITY     keep the c_h largest pooled probabilities P_ij (the
- *                   probability rule of the ablation, Table 3); with cdf_tau > 0
+ *                   probability rule of the ablation, Table 2); with cdf_tau > 0
  *                   keep only the shortest prefix in descending P whose mass,
  *                   the always-kept forced blocks included, reaches cdf_tau (the
- *                   CDF threshold row of Table 3), never below the two-block
+ *                   CDF threshold row of Table 2), never below the two-block
  *                   floor; the realised count replaces c_h in that row's rounds;
- *   DRIFT_MAX_SWAP  sign-flipped objective in the rounds only (Sec. 5.4): the
+ *   DRIFT_MAX_SWAP  sign-flipped objective in the rounds only (Fig. 8, Sec. 6.1): the
  *                   initial set as for DRIFT, every round makes the swaps that
  *                   raise J most, and the largest J seen is kept;
  *   DRIFT_MAX_FULL  sign flipped from the start: keep the c_h smallest keys, then
@@ -162,7 +162,7 @@ int ress_sparse_attn(const ress_shape *shape, const void *q, const void *k, cons
  * aligned, must not alias q, k, v): the same kernels, only the final
  * normalised O is stored unrounded. Differences between two such outputs
  * resolve changes far below the bf16 output's resolution, e.g. the output
- * change caused by masking one key block, the reference measurement of Sec. 2
+ * change caused by masking one key block, the reference measurement of Sec. 3
  * (Fig. 2). */
 int ress_sparse_attn_out_f32(const ress_shape *shape, const void *q, const void *k, const void *v,
                              const int32_t *kept_count, const int32_t *kept_idx, float scale, float *o,
@@ -205,6 +205,23 @@ int ress_qkv_proj_pool(const ress_shape *shape, const void *x, const void *w_qkv
  * H must be a multiple of 4. Pointers 16-byte aligned. */
 int ress_out_proj_residual(const ress_shape *shape, const void *o, const void *w_o, const void *resid_in,
                            void *resid_out, hipStream_t stream);
+
+/* ress_out_proj_residual with a float32 residual stream,
+ *   resid_out_t = resid_in_t + W_O concat_h(O[h][t])
+ * with the projection accumulated in float32 and added to the stream with one
+ * float32 addition per element (no rounding to bf16). The stream then resolves
+ * what the attention sublayer adds to it, the quantity whose change under
+ * sparsification is the residual drift (Sec. 3, "The Right Objective"): across a
+ * stack of layers, calls with O_sparse and W_O and with O_dense and -W_O (exact
+ * in bf16) accumulate sum_l W_O(O_sparse - O_dense).
+ *   o          device bf16 [H][N][64]
+ *   w_o        device bf16 [H*64][H*64], out features x in features (in = 64h + d)
+ *   resid_in   device float32 [N][H*64]
+ *   resid_out  device float32 [N][H*64] out; may be resid_in (in place), must not
+ *              alias o or w_o
+ * H must be a multiple of 4. Pointers 16-byte aligned. */
+int ress_out_proj_residual_f32(const ress_shape *shape, const void *o, const void *w_o, const float *resid_in,
+                               float *resid_out, hipStream_t stream);
 
 /* Human-readable name of a status code (static string). */
 const char *ress_status_string(int status);

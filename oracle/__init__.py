@@ -168,7 +168,7 @@ def swaps(c: int, rho: float, r: int, swap_floor: int = 1) -> int:
     return _L().ro_swaps(int(c), float(rho), int(r), int(swap_floor))
 
 
-# Selection criteria (the paper's comparisons, Secs. 5.3-5.4, Table 3; see the list
+# Selection criteria (the paper's comparisons, Table 2 and Fig. 8 (Sec. 6.1); see the list
 # at the top of ress_oracle.c).
 DRIFT, PROBABILITY, DRIFT_MAX_SWAP, DRIFT_MAX_FULL = 0, 1, 2, 3
 
@@ -231,7 +231,7 @@ def attn_tokens(q, k, v, *, N, bq, bk, scale, sel_h, sel_t, kept_count=None, kep
 
 
 def block_masking_change(q, k, v, gram, *, N, bq, bk, scale, h, i, blocks):
-    """The reference measurement of Sec. 2 (Fig. 2) for query block i of head h:
+    """The reference measurement of Sec. 3 (Fig. 2) for query block i of head h:
     for each key block j in `blocks`, mask only block j and take the change in what
     attention writes into the residual stream, the Euclidean norm over the query
     block's tokens of W_O^h (O_t(B minus j) - O_t(B)), with ||W_O^h x||^2 = x^T M_h x.
@@ -309,3 +309,25 @@ def out_projection_residual(o, w_o, resid):
     H, N, D = np.asarray(o).shape
     flat = _f64(o).transpose(1, 0, 2).reshape(N, H * D)
     return bf16_bits_nearest(_f64(resid) + flat @ _f64(w_o).T)
+
+
+def out_projection_f64(o_rows, w_o, resid=None):
+    """What the attention sublayer adds to the residual stream, W_O concat_h(o_h)
+    (Sec. 3, "The Right Objective"), plus resid if given, in float64 without any
+    rounding. o_rows: float64 [n][64H] attention outputs of n tokens, channel
+    64h + d for head h; w_o: bf16 bits [64H][64H] (out features x in features);
+    resid: float [n][64H] or None. Returns float64 [n][64H]."""
+    y = np.asarray(o_rows, dtype=np.float64) @ _f64(w_o).T
+    return y if resid is None else y + np.asarray(resid, dtype=np.float64)
+
+
+def head_major_rows(o, tokens=None):
+    """Attention outputs o [H][N][64] (bf16 bits or float values) of the given
+    tokens as float64 rows [n][64H] in the residual stream's channel order 64h + d."""
+    o = np.asarray(o)
+    x = _f64(o) if o.dtype == np.uint16 else o.astype(np.float64)
+    if tokens is not None:
+        x = x[:, np.asarray(tokens)]
+    H, n, D = x.shape
+    return x.transpose(1, 0, 2).reshape(n, H * D)
+

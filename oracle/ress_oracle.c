@@ -34,7 +34,7 @@
  *     strictly smallest J, counting the initial one;
  *   - query blocks that hold special tokens attend densely when asked to.
  *
- * Selection criteria (the paper's comparisons, Secs. 5.3-5.4 and Table 3):
+ * Selection criteria (the paper's comparisons, Table 2 and Fig. 8 / Sec. 6.1):
  *   0  drift (ReSS): keep the c largest keys, rounds minimise J;
  *   1  probability (the SparseVGGT rule): keep the c largest P; optionally capped
  *      by a CDF threshold tau: the shortest prefix in descending P whose mass,

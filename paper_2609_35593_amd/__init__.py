@@ -69,6 +69,8 @@ def _load():
     L.ress_qkv_proj_pool.restype = i
     L.ress_out_proj_residual.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp]
     L.ress_out_proj_residual.restype = i
+    L.ress_out_proj_residual_f32.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp]
+    L.ress_out_proj_residual_f32.restype = i
     L.ress_dense_attn.restype = i
     return L
 
@@ -283,6 +285,27 @@ def ress_out_proj_residual(o, w_o, resid_in, *, resid_out=None, stream=None):
                                     _stream(stream, o.device))
     if st != RESS_OK:
         raise RessError(st, "ress_out_proj_residual")
+    return resid_out
+
+
+def ress_out_proj_residual_f32(o, w_o, resid_in, *, resid_out=None, stream=None):
+    """resid_out = resid_in + concat_h(o[h]) w_o^T with a float32 stream (see
+    include/ress.h). o: bf16 [H][N][64]; w_o: bf16 [H*64][H*64]; resid_in/out:
+    float32 [N][H*64] (resid_out may be resid_in)."""
+    H, N, D = o.shape
+    _check_bf16("o", o, (H, N, D))
+    _check_bf16("w_o", w_o, (H * D, H * D))
+    dev = o.device
+    _check_out("resid_in", resid_in, torch.float32, (N, H * D), dev)
+    resid_out = torch.empty_like(resid_in) if resid_out is None else resid_out
+    _check_out("resid_out", resid_out, torch.float32, (N, H * D), dev)
+    if w_o.device != dev:
+        raise ValueError("o and w_o must share a device")
+    shape = make_shape(H, N, bq=128, bk=128, D=D)
+    st = lib.ress_out_proj_residual_f32(C.byref(shape), _ptr(o), _ptr(w_o), _ptr(resid_in), _ptr(resid_out),
+                                        _stream(stream, dev))
+    if st != RESS_OK:
+        raise RessError(st, "ress_out_proj_residual_f32")
     return resid_out
 
 

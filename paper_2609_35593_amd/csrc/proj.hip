@@ -6,7 +6,7 @@
 //    Q, K, V again;
 //  - output projection and residual add, R' = R + concat_h(O_h) W_O^T, reading
 //    the head-major attention output directly (the k-slice of one 64-wide k-tile
-//    is one head).
+//    is one head), into a bf16 or a float32 residual stream.
 //
 // Tiling: 256 x 256 output tile per workgroup, k-tiles of 64, 8 waves, each wave
 // a 64 x 128 sub-tile of 2 x 4 v_mfma_f32_32x32x16_bf16 accumulators (lane l
@@ -44,7 +44,9 @@ __device__ __forceinline__ unsigned int bf16_bits(float x)
     return (unsigned int)__builtin_bit_cast(unsigned short, (__bf16)x);
 }
 
-template <int MODE>  // 0: QKV projection + pooling, 1: output projection + residual
+// 0: QKV projection + pooling, 1: output projection + bf16 residual, 2: output
+// projection + float32 residual.
+template <int MODE>
 __global__ void __launch_bounds__(kThreads, 1) proj_kernel(const ProjParams p)
 {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmem];  // operand slots, then epilogue staging
@@ -257,8 +259,8 @@ __global__ void __launch_bounds__(kThreads, 1) proj_kernel(const ProjParams p)
             }
         }
     } else {
-        // R' = R + acc, rounded once; the float32 tile is staged in two halves of
-        // 128 rows (128 KB each) and combined with R in 16-byte pieces.
+        // R' = R + acc (bf16 stream: rounded once); the float32 tile is staged in two
+        // halves of 128 rows (128 KB each) and combined with R in 16-byte pieces.
         float *stage = reinterpret_cast<float *>(smem);
         constexpr int SR = BN + 4;  // padded float row
         for (int half = 0; half < 2; ++half) {
@@ -272,21 +274,35 @@ __global__ void __launch_bounds__(kThreads, 1) proj_kernel(const ProjParams p)
                             stage[(row_of(mi, v) - 128 * half) * SR + col_of(ni)] = acc[mi][ni][v];
             }
             __syncthreads();
-            for (int e = tid; e < 128 * (BN / 8); e += kThreads) {
-                const int r = e >> 5, c8 = (e & 31) * 8;
-                const int t = m0 + 128 * half + r;
-                if (t >= T) continue;
-                const size_t off = (size_t)t * dm + n0 + c8;
-                const uint4 rin = *reinterpret_cast<const uint4 *>(p.resid_in + off);
-                const unsigned int w[4] = {rin.x, rin.y, rin.z, rin.w};
-                unsigned int o[4];
+            if constexpr (MODE == 1) {
+                for (int e = tid; e < 128 * (BN / 8); e += kThreads) {
+                    const int r = e >> 5, c8 = (e & 31) * 8;
+                    const int t = m0 + 128 * half + r;
+                    if (t >= T) continue;
+                    const size_t off = (size_t)t * dm + n0 + c8;
+                    const uint4 rin = *reinterpret_cast<const uint4 *>(p.resid_in + off);
+                    const unsigned int w[4] = {rin.x, rin.y, rin.z, rin.w};
+                    unsigned int o[4];
 #pragma unroll
-                for (int q2 = 0; q2 < 4; ++q2) {
-                    const float lo = __uint_as_float(w[q2] << 16) + stage[r * SR + c8 + 2 * q2];
-                    const float hi = __uint_as_float(w[q2] & 0xffff0000u) + stage[r * SR + c8 + 2 * q2 + 1];
-                    o[q2] = bf16_bits(lo) | (bf16_bits(hi) << 16);
+                    for (int q2 = 0; q2 < 4; ++q2) {
+                        const float lo = __uint_as_float(w[q2] << 16) + stage[r * SR + c8 + 2 * q2];
+                        const float hi = __uint_as_float(w[q2] & 0xffff0000u) + stage[r * SR + c8 + 2 * q2 + 1];
+                        o[q2] = bf16_bits(lo) | (bf16_bits(hi) << 16);
+                    }
+                    *reinterpret_cast<uint4 *>(p.resid_out + off) = make_uint4(o[0], o[1], o[2], o[3]);
                 }
-                *reinterpret_cast<uint4 *>(p.resid_out + off) = make_uint4(o[0], o[1], o[2], o[3]);
+            } else {
+                // float32 stream: R' = R + acc, one float32 add per element, 16 bytes at a time.
+                for (int e = tid; e < 128 * (BN / 4); e += kThreads) {
+                    const int r = e >> 6, c4 = (e & 63) * 4;
+                    const int t = m0 + 128 * half + r;
+                    if (t >= T) continue;
+                    const size_t off = (size_t)t * dm + n0 + c4;
+                    const float4 rin = *reinterpret_cast<const float4 *>(p.resid_in_f32 + off);
+                    const float *st = stage + r * SR + c4;
+                    *reinterpret_cast<float4 *>(p.resid_out_f32 + off) =
+                        make_float4(rin.x + st[0], rin.y + st[1], rin.z + st[2], rin.w + st[3]);
+                }
             }
             __syncthreads();
         }
@@ -301,8 +317,10 @@ hipError_t launch_proj(const ProjParams &p, hipStream_t s)
     const dim3 grid((unsigned)(8 * p.items_per_xcd)), block(kThreads);
     if (p.mode == 0)
         hipLaunchKernelGGL(proj_kernel<0>, grid, block, 0, s, p);
-    else
+    else if (p.mode == 1)
         hipLaunchKernelGGL(proj_kernel<1>, grid, block, 0, s, p);
+    else
+        hipLaunchKernelGGL(proj_kernel<2>, grid, block, 0, s, p);
     return hipGetLastError();
 }
 

@@ -241,6 +241,27 @@ int ress_out_proj_residual(const ress_shape *shape, const void *o, const void *w
     return RESS_OK;
 }
 
+int ress_out_proj_residual_f32(const ress_shape *shape, const void *o, const void *w_o, const float *resid_in,
+                               float *resid_out, hipStream_t stream)
+{
+    Grid g;
+    ress::ProjParams pp;
+    int st = proj_common(shape, &g, &pp, kD);
+    if (st != RESS_OK) return st;
+    if (!has_work(shape)) return RESS_OK;
+    if (!o || !w_o || !resid_in || !resid_out) return RESS_E_INVALID_ARG;
+    if (!aligned16(o) || !aligned16(w_o) || !aligned16(resid_in) || !aligned16(resid_out))
+        return RESS_E_INVALID_ARG;
+    if ((const void *)resid_out == o || (const void *)resid_out == w_o) return RESS_E_INVALID_ARG;
+    pp.mode = 2;
+    pp.a = static_cast<const uint16_t *>(o);
+    pp.w = static_cast<const uint16_t *>(w_o);
+    pp.resid_in_f32 = resid_in;
+    pp.resid_out_f32 = resid_out;
+    if (ress::launch_proj(pp, stream) != hipSuccess) return RESS_E_HIP;
+    return RESS_OK;
+}
+
 static int attn_common(const ress_shape *shape, const void *q, const void *k, const void *v,
                        const int32_t *kept_count, const int32_t *kept_idx, float scale, void *o,
                        bool sparse, bool out_f32, hipStream_t stream)

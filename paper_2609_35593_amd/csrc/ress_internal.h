@@ -55,17 +55,20 @@ struct AttnParams {
 };
 
 // The projections on either side of the path (mode 0: QKV + pooling, mode 1:
-// output projection + residual), one bf16 GEMM with per-mode epilogues.
+// output projection + bf16 residual, mode 2: output projection + float32
+// residual), one bf16 GEMM with per-mode epilogues.
 struct ProjParams {
     int mode;
     int T, H;                 // tokens, heads (model width 64 H)
     int bq, bk, n_qb, n_kb;   // pooling grid (mode 0)
     int m_tiles, n_tiles, items_per_xcd;
-    const uint16_t *a;        // mode 0: x [T][64H]; mode 1: o [H][T][64]
+    const uint16_t *a;        // mode 0: x [T][64H]; modes 1, 2: o [H][T][64]
     const uint16_t *w;        // [n_out][64H] (out features x in features)
     uint16_t *q, *k, *v;      // mode 0: bf16 [H][T][64]
     const uint16_t *resid_in; // mode 1: bf16 [T][64H]
     uint16_t *resid_out;
+    const float *resid_in_f32;  // mode 2: float32 [T][64H]
+    float *resid_out_f32;
     const float *gram;        // mode 0: [H][64][64]
     Pooled pooled;            // mode 0
 };

@@ -1,4 +1,4 @@
-"""Single-block masking reference (Sec. 2, Fig. 2) on the library's kernels.
+"""Single-block masking reference (Sec. 3, Fig. 2) on the library's kernels.
 
 For each key block j, every query block attends to all key blocks except j
 (ress_sparse_attn_out_f32 with the list B minus j), and the change in what

@@ -9,10 +9,13 @@ Tolerances (applied in compare_*):
   kept lists  bit-exact on every row whose oracle decision margin exceeds
               MARGIN (the smallest relative gap of any top-k cut or track-best
               comparison along the row's trajectory); on the other rows the
-              GPU list must still be a valid selection.
+              GPU list must still be a valid selection, and those rows may be
+              at most MAX_EXCLUDED of the compared rows (0 on the five
+              workloads; the stats line reports the count).
 """
 from __future__ import annotations
 
+import functools
 import math
 import sys
 import time
@@ -23,6 +26,7 @@ import oracle
 import synth
 
 MARGIN = 1e-9
+MAX_EXCLUDED = 0.01  # fraction of compared rows allowed below MARGIN
 ATTN_MAX, ATTN_MEAN = 2e-2, 2e-3
 REL_TOL = 1e-3
 
@@ -30,6 +34,19 @@ REL_TOL = 1e-3
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
+
+
+@functools.lru_cache(maxsize=24)
+def stack_layer(layer: int):
+    """Layer `layer` of the 24-layer stack (drawn once per test process)."""
+    return synth.make_config("16v_stack", layer=layer)
+
+
+def stack_w_o_bits(L):
+    """The full output projection of a layer, bf16 bits [1024][1024] (out x in,
+    input channel 64h + d), from the generator's per-head slices W_O^h."""
+    w, _ = synth.draw_w_o(L.H, L.D, L.seed)
+    return synth.f32_to_bf16_bits(w.transpose(1, 0, 2).reshape(w.shape[1], L.H * L.D).astype(np.float32))
 
 
 def device_inputs(L, dev="cuda:0"):
@@ -89,9 +106,11 @@ def rel_err(a, ref, rowwise_scale):
 
 
 def compare_select(L, gpu, ref, rows=None, budgets=None, label="", dense_special_queries=True, criterion=0,
-                   capped=False):
+                   capped=False, max_excluded=MAX_EXCLUDED):
     """gpu: full-layer arrays; ref: oracle outputs for `rows` (flat h*n_qb+i).
-    criterion 2 / 3 maximise the drift, so the returned J is >= the initial one."""
+    criterion 2 / 3 maximise the drift, so the returned J is >= the initial one.
+    At most `max_excluded` of the rows may fall outside the bit-exact kept-list
+    comparison (oracle margin <= MARGIN); the five workloads require 0."""
     budgets = L.budgets if budgets is None else budgets
     R = L.H * L.n_qb
     rows = np.arange(R) if rows is None else np.asarray(rows)
@@ -102,8 +121,12 @@ def compare_select(L, gpu, ref, rows=None, budgets=None, label="", dense_special
     decided = ref["margin"] > MARGIN
     bad = np.flatnonzero(decided & ~same)
     stats = dict(rows=len(rows), checked=int(decided.sum()), identical=int(same.sum()),
-                 identical_frac=float(same.mean()), excluded=float(1 - decided.mean()))
+                 identical_frac=float(same.mean()), excluded=float(1 - decided.mean()),
+                 excluded_rows=int((~decided).sum()), excluded_identical=int((~decided & same).sum()))
     assert bad.size == 0, f"{label}: {bad.size} decided rows differ, first {rows[bad[:5]]}"
+    assert stats["excluded"] <= max_excluded, (
+        f"{label}: {int((~decided).sum())} of {len(rows)} rows have an oracle margin <= {MARGIN} "
+        f"(allowed fraction {max_excluded})")
     out = {}
     if gpu.get("key") is not None and ref.get("key") is not None:
         key_g = gpu["key"].reshape(R, L.n_kb)[rows]
@@ -147,12 +170,18 @@ def compare_attn(L, o_gpu, hs, ts, kept_count=None, kept_idx=None, label=""):
     import torch
 
     o = o_gpu[torch.from_numpy(hs.astype(np.int64)), torch.from_numpy(ts.astype(np.int64))]
-    o = o.float().cpu().numpy().astype(np.float64)
+    return compare_attn_values(L, o.float().cpu().numpy(), hs, ts, kept_count, kept_idx, label)
+
+
+def compare_attn_values(L, o, hs, ts, kept_count=None, kept_idx=None, label=""):
+    """o: the GPU outputs of the (head, token) pairs hs, ts, as float [n][D]."""
+    o = np.asarray(o, np.float64)
     t0 = time.time()
     ref = oracle.attn_tokens(L.q, L.k, L.v, N=L.N, bq=L.bq, bk=L.bk, scale=1.0 / math.sqrt(L.D), sel_h=hs,
                              sel_t=ts, kept_count=kept_count, kept_idx=kept_idx)
     err = np.abs(o - ref)
     say(f"  attn parity {label}: {len(hs)} tokens, max {err.max():.3e}, mean {err.mean():.3e}, "
         f"mean|ref| {np.abs(ref).mean():.3f} (oracle {time.time() - t0:.1f}s)")
+    assert np.all(np.isfinite(o)), (label, "non-finite outputs")
     assert err.max() <= ATTN_MAX and err.mean() <= ATTN_MEAN, (label, err.max(), err.mean())
     return float(err.max()), float(err.mean())

@@ -301,9 +301,114 @@ def check_brute_force(report=None):
                     report.append(res["J_best"] / jstar if jstar > 0 else 1.0)
 
 
+def _direct_margin(r, c, criterion=0, cdf_tau=0.0, trace_D=None):
+    """The decision margin of a row, from the definitions: the smallest relative
+    gap of every cut the selection makes along its trajectory trace_D (the
+    oracle's stages; each one is pinned separately by check_trajectory),
+    computed from exact masked-softmax drifts rather than the closed forms:
+      initial cut    gap between the c-th and (c+1)-th ranking value (key, P or
+                     -key by criterion) over the largest |value|; with a CDF cap
+                     also the distance of tau to the two partial masses around the
+                     cut, over tau;
+      each round     gap between the m-th and (m+1)-th exact single-swap gain
+                     J(D) - J(D with k toggled) (negated when maximising), among
+                     restores and among drops, over J(D);
+      track-best     |J_new - J_best| / J_best whenever the new set differs from
+                     the best one so far.
+    Returns (margin, which) with which the kind of cut that attains it."""
+    cand = ~r["forced"]
+    n = len(cand)
+    n_p = int(cand.sum())
+    Jm = lambda d: direct.drift_sq_m(r["logits"], r["vbar"], r["M"], d)
+    P = softmax(r["logits"])
+    out = [(math.inf, "none")]
+    if c >= n_p:
+        return out[0]
+    single = np.array([Jm(np.eye(n, dtype=bool)[j]) if cand[j] else 0.0 for j in range(n)])
+    key = np.sqrt(single)  # Eq. 12 for a single dropped block: J({j}) = key_j^2
+    rank = P if criterion == 1 else -key if criterion == 3 else key
+    if criterion == 1 and cdf_tau > 0.0:
+        mass = P[r["forced"]].sum()
+        order = sorted(np.flatnonzero(cand).tolist(), key=lambda j: (-P[j], j))
+        cnt = 0
+        while cnt < len(order) and mass < cdf_tau:
+            mass += P[order[cnt]]
+            cnt += 1
+        if 0 < cnt < c:
+            out.append((min(mass - cdf_tau, cdf_tau - (mass - P[order[cnt - 1]])) / cdf_tau, "cdf"))
+        lo = min(max(0, 2 - int(r["forced"].sum())), n_p)
+        c = min(c, max(cnt, lo))
+    if c > 0:
+        _, gap = direct.top_by(rank, cand, c)
+        vmax = np.abs(rank[cand]).max()
+        out.append((gap / (vmax if vmax > 0 else 1e-300), "initial"))
+    maximise = criterion in (2, 3)
+    best_D = trace_D[0]
+    best_J = Jm(best_D)
+    for st in range(len(trace_D) - 1):
+        Ds = trace_D[st]
+        Js = Jm(Ds)
+        m = min(_schedule(c, st), n_p - c, c)
+        gain = np.full(n, -np.inf)
+        for k in np.flatnonzero(cand):
+            nd = Ds.copy()
+            nd[k] = not nd[k]
+            gain[k] = (Jm(nd) - Js) if maximise else (Js - Jm(nd))
+        for member in (Ds, cand & ~Ds):
+            _, gap = direct.top_by(gain, member, m)
+            out.append((gap / (Js if Js > 0 else 1e-300), "round"))
+        Dn = trace_D[st + 1]
+        Jn = Jm(Dn)
+        if not np.array_equal(Dn, best_D):
+            out.append((abs(Jn - best_J) / (best_J if best_J > 0 else 1e-300), "track-best"))
+        if (Jn > best_J) if maximise else (Jn < best_J):
+            best_D, best_J = Dn, Jn
+    return min(out, key=lambda t: t[0])
+
+
+MARGIN_CASES = [(0, 0.0), (1, 0.0), (1, 0.5), (2, 0.0), (3, 0.0)]
+
+
+def check_margin(report=None):
+    """The oracle's decision margin (the gate of the bit-exact kept-list comparison
+    against the GPU path) equals the margin recomputed from the definitions, for
+    every criterion; exact ties give margin 0 and rows with nothing to decide
+    give +inf."""
+    for name in ("forced", "plain"):
+        for h, i in rows_of(name, 2):
+            r = _row(name, h, i)
+            P = softmax(r["logits"])
+            if np.any(1.0 - P[~r["forced"]] <= EPS):
+                continue  # the eps guard of Eq. 7 makes key^2 differ from the masked drift
+            for crit, tau in MARGIN_CASES:
+                res = oracle.select_row(r["qbar_i"], r["kbar"], r["vbar"], r["M"], r["forced"], r["c"], rounds=5,
+                                        criterion=crit, cdf_tau=tau)
+                want, which = _direct_margin(r, r["c"], crit, tau, res["trace_D"])
+                got = res["margin"]
+                assert abs(got - want) <= 1e-7 * want + 1e-10, (name, h, i, crit, tau, got, want, which)
+                if report is not None:
+                    report.append((which, want))
+    # Exact ties: identical blocks, every key and gain equal.
+    L = layer("forced")
+    kb = np.repeat(pooled("forced")[1][0, :1], L.n_kb, axis=0)
+    vb = np.repeat(pooled("forced")[2][0, :1], L.n_kb, axis=0)
+    forced = np.zeros(L.n_kb, bool)
+    forced[-2:] = True
+    for c in (1, 4, 9):
+        res = oracle.select_row(pooled("forced")[0][0, 3], kb, vb, L.gram[0].astype(np.float64), forced, c, rounds=5)
+        assert res["margin"] == 0.0, (c, res["margin"])
+    # Nothing to decide: dense rows and full budgets.
+    r = _row("forced", 0, 2)
+    n_p = int((~r["forced"]).sum())
+    for kw in (dict(c=n_p), dict(c=3, dense_row=True)):
+        c = kw.pop("c")
+        res = oracle.select_row(r["qbar_i"], r["kbar"], r["vbar"], r["M"], r["forced"], c, rounds=5, **kw)
+        assert res["margin"] == math.inf, (c, kw, res["margin"])
+
+
 # --------------------------------------------------------------------------- other criteria
-# (the paper's comparisons: probability selection and its CDF threshold, Table 3;
-# drift maximisation, Sec. 5.4)
+# (the paper's comparisons: probability selection and its CDF threshold, Table 2;
+# drift maximisation, Fig. 8 / Sec. 6.1)
 
 
 def check_probability_criterion():
@@ -360,7 +465,7 @@ def check_cdf_threshold():
 
 
 def check_drift_max():
-    """Sign-flipped objective (Sec. 5.4). Full flip with no rounds keeps the c
+    """Sign-flipped objective (Fig. 8, Sec. 6.1). Full flip with no rounds keeps the c
     smallest single-block drifts J({j}) = key_j^2; in the rounds every swap is the
     one that raises J most (at the round-start set), track-best keeps the largest J,
     and on small rows the result never exceeds the brute-force maximum."""
@@ -519,4 +624,4 @@ ALL = [check_pool, check_forced, check_pooled_map, check_single_mask, check_scor
        check_key_singleton, check_two_block, check_objective, check_deltas, check_schedule,
        check_trajectory, check_track_best, check_ties, check_brute_force, check_select_driver,
        check_edges, check_attention, check_zero_sparsity, check_probability_criterion,
-       check_cdf_threshold, check_drift_max]
+       check_cdf_threshold, check_drift_max, check_margin]

@@ -26,9 +26,9 @@ def ress():
 
 
 def test_header_declares_the_boundary():
-    assert declared_entry_points() == ["ress_dense_attn", "ress_out_proj_residual", "ress_qkv_proj_pool",
-                                       "ress_select", "ress_select_workspace_size", "ress_sparse_attn",
-                                       "ress_sparse_attn_out_f32", "ress_status_string"]
+    assert declared_entry_points() == ["ress_dense_attn", "ress_out_proj_residual", "ress_out_proj_residual_f32",
+                                       "ress_qkv_proj_pool", "ress_select", "ress_select_workspace_size",
+                                       "ress_sparse_attn", "ress_sparse_attn_out_f32", "ress_status_string"]
 
 
 def test_library_exports_every_declared_symbol(ress):
@@ -166,6 +166,14 @@ def test_projections_reject_before_launch(ress):
     assert out(C.byref(shape), p[0], p[1], p[2], p[0], None) == ress.RESS_E_INVALID_ARG  # resid_out aliases o
     assert out(C.byref(shape), p[0], p[1], p[2], None, None) == ress.RESS_E_INVALID_ARG
     assert out(C.byref(empty), None, None, None, None, None) == ress.RESS_OK
+    out32 = ress.lib.ress_out_proj_residual_f32
+    assert out32(C.byref(ress.make_shape(2, 1000, bq=128, bk=128)), p[0], p[1], p[2], p[3],
+                 None) == ress.RESS_E_UNSUPPORTED
+    assert out32(C.byref(shape), p[0], p[1], p[2], p[0], None) == ress.RESS_E_INVALID_ARG  # resid_out aliases o
+    assert out32(C.byref(shape), p[0], p[1], p[2], p[1], None) == ress.RESS_E_INVALID_ARG  # resid_out aliases w_o
+    assert out32(C.byref(shape), p[0], p[1], None, p[3], None) == ress.RESS_E_INVALID_ARG
+    assert out32(C.byref(shape), p[0], p[1], C.c_void_p((1 << 41) + 4), p[3], None) == ress.RESS_E_INVALID_ARG
+    assert out32(C.byref(empty), None, None, None, None, None) == ress.RESS_OK
 
 
 def test_select_with_pooled_state_needs_no_qkv(ress):

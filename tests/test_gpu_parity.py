@@ -7,8 +7,8 @@ import numpy as np
 import pytest
 
 import synth
-from gpu_helpers import (compare_attn, compare_select, device_inputs, gpu_select, oracle_select,
-                         sample_tokens, say)
+from gpu_helpers import (compare_attn, compare_attn_values, compare_select, device_inputs, gpu_select,
+                         oracle_select, sample_tokens, say, stack_layer)
 
 pytestmark = pytest.mark.gpu
 
@@ -88,7 +88,7 @@ def test_select_budgets_and_rounds(ress, rounds, frac):
     compare_select(L, gpu, ref, budgets=budgets, label=f"R={rounds} frac={frac}")
 
 
-CRITERIA = [  # (criterion, cdf_tau, rounds): the paper's comparisons, Table 3 and Sec. 5.4
+CRITERIA = [  # (criterion, cdf_tau, rounds): the paper's comparisons, Table 2 and Fig. 8
     (1, 0.0, 0), (1, 0.0, 5), (1, 0.7, 0), (1, 0.9, 3), (2, 0.0, 5), (3, 0.0, 0), (3, 0.0, 5)]
 
 
@@ -140,14 +140,19 @@ def test_zero_sparsity_sparse_equals_dense(ress):
 
 
 def _logit_range_layer():
-    """Four heads whose query rows sit at different logit ranges: head 0 as drawn
+    """Heads whose query rows sit at different logit ranges: head 0 as drawn
     (natural logits up to ~15), head 1 with every query scaled by 6 (up to ~100),
     head 2 with every fifth query scaled by 6 (waves that mix both ranges), head 3
     with keys along a shared direction and queries against it (every row's
-    largest logit near -36, about -52 in base 2)."""
+    largest logit near -36, about -52 in base 2). Heads 4-6 put every row's
+    largest base-2 logit below -128, where exp2 of a logit underflows float32
+    and the kernel must move the row's reference down before it has any mass:
+    head 4 near -159 throughout; head 5 near -238 on the first third of the keys
+    and near -159 after (the reference falls, then rises); head 6 near -159 on
+    the first third and near +60 after (a jump of ~220 in base 2)."""
     import dataclasses
 
-    L = synth.make_layer(2, 700, 5, H=4, block=128, sparsity=0.5, seed=31, name="logit-ranges")
+    L = synth.make_layer(2, 700, 5, H=7, block=128, sparsity=0.5, seed=31, name="logit-ranges")
     q = synth.bf16_bits_to_f32(L.q).astype(np.float64)
     k = synth.bf16_bits_to_f32(L.k).astype(np.float64)
     q[1] *= 6.0
@@ -155,17 +160,37 @@ def _logit_range_layer():
     u = np.full(64, 1.0 / 8.0)  # unit vector
     k[3] = 0.25 * k[3] + 4.0 * u
     q[3] = 0.25 * q[3] - 80.0 * u
+    early = np.arange(L.N) < L.N // 3
+    for h, (a_early, a_late) in ((4, (4.0, 4.0)), (5, (6.0, 4.0)), (6, (4.0, -1.5))):
+        a = np.where(early, a_early, a_late)[:, None]
+        k[h] = 0.25 * k[h] + a * u
+        q[h] = 0.25 * q[h] - 220.0 * u
     return dataclasses.replace(L, q=synth.f32_to_bf16_bits(q.astype(np.float32)),
                                k=synth.f32_to_bf16_bits(k.astype(np.float32)))
 
 
+def _row_max_logit2(L):
+    """Largest base-2 logit of every (head, query token) over all keys."""
+    q = synth.bf16_bits_to_f32(L.q).astype(np.float64)
+    k = synth.bf16_bits_to_f32(L.k).astype(np.float64)
+    return np.stack([(q[h] @ k[h].T).max(axis=1) for h in range(L.H)]) / 8.0 / math.log(2.0)
+
+
 def test_attention_logit_ranges(ress):
     """Dense and sparse attention where rows leave the band in which the kernel
-    forms probabilities without a reference subtraction, at the same tolerance."""
+    forms probabilities without a reference subtraction, at the same tolerance;
+    every output finite."""
+    import dataclasses
+
     import torch
 
     L = _logit_range_layer()
-    say(f"[logit ranges] H={L.H} N={L.N}")
+    mx = _row_max_logit2(L)
+    early = _row_max_logit2(dataclasses.replace(L, N=L.N // 3, k=L.k[:, :L.N // 3]))
+    # Every key block visited first (ascending lists) starts below -128 on heads 4-6.
+    assert np.all(mx[4:6] < -128) and np.all(early[4:] < -128) and mx[1].max() > 100
+    say(f"[logit ranges] H={L.H} N={L.N}; row maxima (base 2) per head "
+        f"{[(round(float(m.min())), round(float(m.max()))) for m in mx]}")
     inputs = device_inputs(L)
     q, k, v, _ = inputs
     hs, ts = _all_tokens(L)
@@ -178,7 +203,7 @@ def test_attention_logit_ranges(ress):
 
 
 def test_block_masking_change(ress):
-    """Sec. 2's single-block masking reference through ress_sparse_attn_out_f32
+    """Sec. 3's single-block masking reference through ress_sparse_attn_out_f32
     against the oracle, for rows of every head (first, middle, special tail),
     every key block; and the Spearman correlations it feeds."""
     import torch
@@ -210,21 +235,41 @@ def test_block_masking_change(ress):
 
 # ------------------------------------------------------------------ the five workloads
 
+# GPU results of the last full-size layer run, shared by the tests that check its
+# rows in chunks: (key, L, selection arrays, sampled attention outputs, tokens).
+_LAST = {}
 
-def _config_case(ress, L, rounds, rows=None, n_tokens=512, label=""):
+
+def _gpu_layer(ress, key, L, rounds, n_tokens):
     import torch
 
-    say(f"[{label}] H={L.H} N={L.N} n_qb={L.n_qb} n_kb={L.n_kb} R={rounds} "
-        f"budgets={sorted(set(L.budgets.tolist()))[:6]}")
-    inputs = device_inputs(L)
-    gpu, dev = gpu_select(L, inputs, rounds=rounds)
+    if _LAST.get("key") != key:
+        _LAST.clear()
+        say(f"[{key}] GPU run: H={L.H} N={L.N} n_qb={L.n_qb} n_kb={L.n_kb} R={rounds} "
+            f"budgets={sorted(set(L.budgets.tolist()))[:6]}")
+        inputs = device_inputs(L)
+        gpu, dev = gpu_select(L, inputs, rounds=rounds)
+        q, k, v, _ = inputs
+        o = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk)
+        torch.cuda.synchronize()
+        hs, ts = sample_tokens(L, n_tokens)
+        o_s = o[torch.from_numpy(hs.astype(np.int64)), torch.from_numpy(ts.astype(np.int64))]
+        _LAST.update(key=key, L=L, gpu=gpu, o=o_s.float().cpu().numpy(), hs=hs, ts=ts)
+        del inputs, dev, o
+        torch.cuda.empty_cache()
+    return _LAST
+
+
+def _config_case(ress, L, rounds, rows=None, n_tokens=512, label="", check_attn=True, max_excluded=0.0):
+    """Selection of `rows` (every row if None) against the oracle, no row (or at most
+    `max_excluded` of them) outside the bit-exact kept-list comparison; sparse
+    attention on sampled tokens."""
+    c = _gpu_layer(ress, label.split(" chunk")[0], L, rounds, n_tokens)
     ref = oracle_select(L, rounds=rounds, rows=rows)
-    st = compare_select(L, gpu, ref, rows=rows, label=label)
-    q, k, v, _ = inputs
-    o = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk)
-    torch.cuda.synchronize()
-    hs, ts = sample_tokens(L, n_tokens)
-    compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label=label + " sparse")
+    st = compare_select(L, c["gpu"], ref, rows=rows, label=label, max_excluded=max_excluded)
+    if check_attn:
+        compare_attn_values(L, c["o"], c["hs"], c["ts"], kept_count=c["gpu"]["kept_count"],
+                            kept_idx=c["gpu"]["kept_idx"], label=label + " sparse")
     return st
 
 
@@ -241,23 +286,36 @@ def test_config_32v(ress, sparsity, rounds):
 def test_config_32v_q128_k64(ress):
     """The paper's own grid: 128-token query blocks, 64-token key blocks (687 key
     blocks per head at 32 views, so 12 slots per lane in the selection and two
-    kept blocks per 128-key attention tile). Oracle on a row sample."""
+    kept blocks per 128-key attention tile). Every row."""
     L = synth.make_config("32v", sparsity=0.75, bk=64)
     assert (L.bq, L.bk, L.n_kb) == (128, 64, 687)
-    rng = np.random.default_rng(11)
-    rows = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 600),
-                                     [h * L.n_qb + i for h in range(L.H) for i in (0, L.n_qb - 1, L.n_qb - 2)]]))
-    _config_case(ress, L, 5, rows=rows, n_tokens=384, label="32v q128/k64")
+    _config_case(ress, L, 5, n_tokens=384, label="32v q128/k64")
 
 
 def test_select_one_row_per_wave_range(ress):
     """385-768 key blocks run one row per wave (8 slots per lane here): 22 views on
-    the 128/64 grid, 473 key blocks, oracle on a row sample."""
+    the 128/64 grid, 473 key blocks, every row."""
     L = synth.make_layer(22, 1369, 5, H=4, bq=128, bk=64, sparsity=0.8, seed=33, name="22v q128/k64")
     assert 384 < L.n_kb <= 512
-    rng = np.random.default_rng(12)
-    rows = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 300), [L.n_qb - 1, 0]]))
-    _config_case(ress, L, 5, rows=rows, n_tokens=256, label="22v q128/k64")
+    _config_case(ress, L, 5, n_tokens=256, label="22v q128/k64")
+
+
+@pytest.mark.parametrize("chunk", range(4))
+def test_config_100v_ragged(ress, chunk):
+    """100 views, per-head budgets drawn from [80%, 95%] sparsity: every row, in
+    four interleaved chunks against one GPU run."""
+    L = synth.make_config("100v")
+    rows = np.arange(L.H * L.n_qb)[chunk::4]
+    # Two of the 17,184 rows are near-ties by the oracle's own margin (~3e-11 and
+    # ~1e-10 relative, below the 1e-9 gate): at most those two may be excluded.
+    _config_case(ress, L, 5, rows=rows, n_tokens=256, label=f"100v ragged chunk {chunk}", check_attn=chunk == 0,
+                 max_excluded=2.5 / len(rows))
+
+
+@pytest.mark.parametrize("layer", range(24))
+def test_config_layer_stack(ress, layer):
+    """Every layer of the 24-layer stack (noise rising 0.3 -> 1.0), every row."""
+    _config_case(ress, stack_layer(layer), 5, n_tokens=128, label=f"16v layer {layer}")
 
 
 def _rows_per_wave(H, n_qb, n_kb):
@@ -294,19 +352,6 @@ def test_select_launch_shapes(ress, views, ppv, H, cpl, rpw):
     gpu, _ = gpu_select(L, rounds=3, criterion=1, cdf_tau=0.25)  # the cap binds on most rows here
     compare_select(L, gpu, oracle_select(L, rounds=3, rows=rows, criterion=1, cdf_tau=0.25), rows=rows,
                    label=f"{cpl}x{rpw} cdf", criterion=1, capped=True)
-
-
-def test_config_100v_ragged(ress):
-    L = synth.make_config("100v")
-    rng = np.random.default_rng(5)
-    rows = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 400),
-                                     [h * L.n_qb + i for h in range(L.H) for i in (0, L.n_qb - 1, L.n_qb - 6)]]))
-    _config_case(ress, L, 5, rows=rows, n_tokens=256, label="100v ragged")
-
-
-@pytest.mark.parametrize("layer", [0, 7, 15, 23])
-def test_config_layer_stack(ress, layer):
-    _config_case(ress, synth.make_config("16v_stack", layer=layer), 5, n_tokens=256, label=f"16v layer {layer}")
 
 
 def test_dense_attention_32v_sampled(ress):
@@ -435,20 +480,29 @@ def test_empty_shapes_are_no_ops(ress):
     torch.cuda.synchronize()
 
 
-def test_key_block_cap(ress):
-    """n_kb = 4096 (the register-row cap) works; sampled rows against the oracle."""
-    L = synth.make_layer(4096 * 128 // 1374 + 1, 1369, 5, H=1, block=128, sparsity=0.9, seed=31, name="cap")
-    if L.n_kb > 4096:  # trim to exactly 4096 blocks
-        N = 4096 * 128
-        cut = L.N - N  # drop leading patch tokens; the special tail stays
-        L = synth.Layer(H=1, N=N, D=64, bq=128, bk=128, n_special_tail=L.n_special_tail,
-                        q=np.ascontiguousarray(L.q[:, cut:]), k=np.ascontiguousarray(L.k[:, cut:]),
-                        v=np.ascontiguousarray(L.v[:, cut:]), gram=L.gram,
-                        budgets=synth.budgets_from_sparsity([0.9], N, 128, L.n_special_tail),
-                        sparsity=np.array([0.9]), seed=31, name="cap")
+def _cap_layer(bq, bk, sparsity, seed):
+    """A one-head layer with exactly 4096 key blocks (the register-row cap):
+    VGGT-shaped views with the leading patch tokens trimmed, the special tail kept."""
+    views = 4096 * bk // 1374 + 1
+    L = synth.make_layer(views, 1369, 5, H=1, bq=bq, bk=bk, sparsity=sparsity, seed=seed, name="cap")
+    N = 4096 * bk
+    cut = L.N - N  # drop leading patch tokens; the special tail stays
+    assert cut >= 0
+    L = synth.Layer(H=1, N=N, D=64, bq=bq, bk=bk, n_special_tail=L.n_special_tail,
+                    q=np.ascontiguousarray(L.q[:, cut:]), k=np.ascontiguousarray(L.k[:, cut:]),
+                    v=np.ascontiguousarray(L.v[:, cut:]), gram=L.gram,
+                    budgets=synth.budgets_from_sparsity([sparsity], N, bk, L.n_special_tail),
+                    sparsity=np.array([sparsity]), seed=seed, name="cap")
     assert L.n_kb == 4096
-    rows = np.array([0, 1, 2047, 4093, 4094, 4095])
-    say(f"[cap] n_kb={L.n_kb} budgets={L.budgets.tolist()} rows={rows.tolist()}")
-    gpu, _ = gpu_select(L, rounds=5)
-    ref = oracle_select(L, rounds=5, rows=rows)
-    compare_select(L, gpu, ref, rows=rows, label="n_kb=4096")
+    return L
+
+
+@pytest.mark.parametrize("bq,bk", [(128, 128), (128, 64)])
+def test_key_block_cap(ress, bq, bk):
+    """n_kb = 4096 (the register-row cap, Supp. E) on both grids: selection of ~1000
+    sampled rows (first, last, special) against the oracle, and block-sparse
+    attention on sampled tokens."""
+    L = _cap_layer(bq, bk, 0.9, 31 + bk)
+    rng = np.random.default_rng(bk)
+    rows = np.unique(np.concatenate([rng.integers(0, L.n_qb, 1000), [0, 1, L.n_qb // 2, L.n_qb - 2, L.n_qb - 1]]))
+    _config_case(ress, L, 5, rows=rows, n_tokens=256, label=f"n_kb=4096 q{bq}/k{bk}", max_excluded=0.01)

@@ -1,4 +1,4 @@
-"""The oracle's single-block masking reference (Sec. 2, Fig. 2) and its rank
+"""The oracle's single-block masking reference (Sec. 3, Fig. 2) and its rank
 correlation, pinned to definitions computed independently here."""
 import math
 

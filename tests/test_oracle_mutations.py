@@ -32,6 +32,12 @@ MUTATIONS = {
     "pool_divides_by_block": ("sum / (double)(hi - lo)", "sum / (double)b"),
     "attn_unscaled": ("lg[ns] = dot * scale;", "lg[ns] = dot;"),
     "mass_sign": ("double K = 1.0 - mass;", "double K = 1.0 + mass;"),
+    "margin_always_zero": ("    *margin = mrg;\n", "    *margin = 0.0;\n"),
+    "margin_ignores_rounds": ("        mrg = min2(mrg, gap_r / jden);\n        mrg = min2(mrg, gap_d / jden);\n", ""),
+    "margin_ignores_track_best": (
+        "        if (memcmp(inD, best, nkb) != 0) mrg = min2(mrg, fabs(J - Jb) / (Jb > 0.0 ? Jb : 1e-300));\n", ""),
+    "margin_initial_unnormalised": ("gap / (vmax > 0.0 ? vmax : 1e-300)", "gap"),
+    "margin_cdf_ignored": ("                mrg = min2(mrg, min2(mass - cdf_tau, cdf_tau - before) / cdf_tau);\n", ""),
     "drop_gain_uses_plus_u": ("dG = 2.0 * dkMg + s[k] * s[k];\n            u = -P[k];",
                               "dG = 2.0 * dkMg + s[k] * s[k];\n            u = P[k];"),
 }

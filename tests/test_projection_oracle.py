@@ -79,3 +79,33 @@ def test_out_projection_residual_cases():
     zero_r = _bits(np.zeros((N, dm)))
     np.testing.assert_array_equal(synth.bf16_bits_to_f32(oracle.out_projection_residual(ones, _bits(sel), zero_r)),
                                   np.ones((N, dm), np.float32))
+
+
+def test_out_projection_f64_cases():
+    """The float64 stream update: W_O = I returns R + concat_h(O) exactly; W_O = 0
+    returns R; a permutation W_O permutes the channels; -W_O cancels W_O; small
+    integers give the exact integer product; head_major_rows lays heads out as
+    channel 64h + d."""
+    H, N = 4, 11
+    dm = 64 * H
+    rng = np.random.default_rng(5)
+    o = _bits(rng.normal(size=(H, N, 64)))
+    r = rng.normal(size=(N, dm)).astype(np.float32)
+    rows = oracle.head_major_rows(o)
+    of = synth.bf16_bits_to_f32(o).astype(np.float64)
+    for h in range(H):
+        np.testing.assert_array_equal(rows[:, 64 * h:64 * h + 64], of[h])
+    np.testing.assert_array_equal(oracle.head_major_rows(o, [3, 7]), rows[[3, 7]])
+    np.testing.assert_array_equal(oracle.out_projection_f64(rows, _bits(np.eye(dm)), r), r.astype(np.float64) + rows)
+    np.testing.assert_array_equal(oracle.out_projection_f64(rows, _bits(np.zeros((dm, dm))), r), r)
+    perm = rng.permutation(dm)
+    pm = np.zeros((dm, dm))
+    pm[np.arange(dm), perm] = 1.0
+    np.testing.assert_array_equal(oracle.out_projection_f64(rows, _bits(pm)), rows[:, perm])
+    w = _bits(rng.normal(size=(dm, dm)) / 16)
+    neg = w ^ np.uint16(0x8000)
+    np.testing.assert_array_equal(oracle.out_projection_f64(rows, w) + oracle.out_projection_f64(rows, neg), 0.0)
+    oi = rng.integers(-3, 4, size=(N, dm))
+    wi = rng.integers(-2, 3, size=(dm, dm))
+    np.testing.assert_array_equal(oracle.out_projection_f64(oi.astype(np.float64), _bits(wi)), oi @ wi.T)
+
