@@ -139,6 +139,24 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
                 int32_t *kept_count, int32_t *kept_idx, double *drift, double *key_out,
                 double *prob_out, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): ress_select without a
+ * caller workspace. The pooled state lives in a fixed device array inside the
+ * library, RESS_NOALLOC_SCRATCH_BYTES per GPU, created with the library's code
+ * object on each GPU it runs on and held until the process ends; this call
+ * allocates and frees nothing. The current device's array is used (the stream
+ * must belong to the current device). Every call on one GPU shares that GPU's
+ * array, which keeps the last call's contents: calls that overlap on one GPU
+ * (other streams, other threads) race, and the caller must serialise them.
+ * Arguments and results as ress_select; params->pooled_in_workspace must be 0
+ * (RESS_E_INVALID_ARG otherwise); shapes whose workspace
+ * (ress_select_workspace_size) exceeds RESS_NOALLOC_SCRATCH_BYTES return
+ * RESS_E_UNSUPPORTED (the 100-view layer, 16 heads x 1074 blocks, needs 35 MB). */
+#define RESS_NOALLOC_SCRATCH_BYTES (48u << 20)
+int ress_select_noalloc(const ress_shape *shape, const ress_select_params *params, const void *q, const void *k,
+                        const void *v, const float *gram, const int32_t *keep_budget, int32_t *kept_count,
+                        int32_t *kept_idx, double *drift, double *key_out, double *prob_out, hipStream_t stream);
+
 /* Block-sparse attention (Sec. 3 step (3)): every query token t of query block
  * i attends exactly to the tokens of the key blocks kept_idx[h][i][0 ..
  * kept_count[h][i]-1], with the softmax renormalised among them:

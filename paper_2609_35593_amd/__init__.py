@@ -24,6 +24,7 @@ RESS_E_UNSUPPORTED = -2
 RESS_E_WORKSPACE = -3
 RESS_E_HIP = -4
 MAX_KEY_BLOCKS = 4096
+NOALLOC_SCRATCH_BYTES = 48 << 20
 
 
 class ress_shape(C.Structure):
@@ -60,6 +61,9 @@ def _load():
     L.ress_select.argtypes = [C.POINTER(ress_shape), C.POINTER(ress_select_params), vp, vp, vp, vp, vp, vp, vp,
                               vp, vp, vp, vp, sz, vp]
     L.ress_select.restype = i
+    L.ress_select_noalloc.argtypes = [C.POINTER(ress_shape), C.POINTER(ress_select_params), vp, vp, vp, vp, vp, vp,
+                                      vp, vp, vp, vp, vp]
+    L.ress_select_noalloc.restype = i
     L.ress_sparse_attn.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, f, vp, vp]
     L.ress_sparse_attn.restype = i
     L.ress_sparse_attn_out_f32.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, f, vp, vp]
@@ -178,6 +182,38 @@ def ress_select(q, k, v, gram, keep_budget, *, bq: int, bk: int, n_special_tail:
                          _ptr(prob_out), _ptr(workspace), ws_bytes, _stream(stream, dev))
     if st != RESS_OK:
         raise RessError(st, "ress_select")
+    return dict(kept_count=kept_count, kept_idx=kept_idx, drift=drift, key=key_out, prob=prob_out)
+
+
+def ress_select_noalloc(q, k, v, gram, keep_budget, *, bq: int, bk: int, kept_count, kept_idx,
+                        n_special_tail: int = 0, rounds: int = 5, rho: float = 0.5, eps: float = 1e-4,
+                        swap_floor: int = 1, dense_special_queries: bool = True, criterion: int = CRITERION_DRIFT,
+                        cdf_tau: float = 0.0, drift=None, key_out=None, prob_out=None, stream=None) -> dict:
+    """ress_select with the library's fixed per-GPU scratch instead of a workspace
+    (see include/ress.h): neither this binding nor the library allocates; every
+    output is the caller's."""
+    _check_qkv(q, k, v)
+    H, N, D = q.shape
+    shape = make_shape(H, N, bq=bq, bk=bk, n_special_tail=n_special_tail, D=D)
+    n_qb, n_kb = (N + bq - 1) // bq, (N + bk - 1) // bk
+    dev = q.device
+    _check_out("gram", gram, torch.float32, (H, D, D), dev)
+    budget = np.ascontiguousarray(np.asarray(keep_budget, dtype=np.int32).reshape(-1))
+    if budget.shape[0] != H:
+        raise ValueError("keep_budget must hold one int per head")
+    _check_out("kept_count", kept_count, torch.int32, (H, n_qb), dev)
+    _check_out("kept_idx", kept_idx, torch.int32, (H, n_qb, n_kb), dev)
+    for name, t, shp in (("drift", drift, (H, n_qb, 2)), ("key_out", key_out, (H, n_qb, n_kb)),
+                         ("prob_out", prob_out, (H, n_qb, n_kb))):
+        if t is not None:
+            _check_out(name, t, torch.float64, shp, dev)
+    params = ress_select_params(int(rounds), float(rho), float(eps), int(swap_floor), int(bool(dense_special_queries)),
+                                int(criterion), float(cdf_tau), 0)
+    st = lib.ress_select_noalloc(C.byref(shape), C.byref(params), _ptr(q), _ptr(k), _ptr(v), _ptr(gram),
+                                 budget.ctypes.data, _ptr(kept_count), _ptr(kept_idx), _ptr(drift), _ptr(key_out),
+                                 _ptr(prob_out), _stream(stream, dev))
+    if st != RESS_OK:
+        raise RessError(st, "ress_select_noalloc")
     return dict(kept_count=kept_count, kept_idx=kept_idx, drift=drift, key=key_out, prob=prob_out)
 
 

@@ -4,7 +4,15 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "ress_internal.h"
+
+// Device memory of ress_select_noalloc: the selection's workspace for callers that
+// cannot allocate. One copy per GPU (at its own address), held until the process
+// ends; host code never passes this name to a kernel, only the per-device address
+// hipGetSymbolAddress returns for it.
+static __device__ __align__(256) unsigned char scratch[RESS_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -54,6 +62,26 @@ ress::Pooled pooled_layout(const ress_shape *s, const Grid &g, void *workspace)
     pooled.vbarT = reinterpret_cast<double *>(w + qb + 2 * kb);
     pooled.cT = reinterpret_cast<double *>(w + qb + 3 * kb);
     return pooled;
+}
+
+// Address of the current device's copy of `scratch`, looked up once per device
+// (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices];
+
+int scratch_of_current_device(void **out)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return RESS_E_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return RESS_E_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return RESS_OK;
 }
 
 int first_forced_block(const ress_shape *s, const Grid &g)
@@ -164,6 +192,25 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
     if (!pooled_ready && ress::launch_pool(pp, stream) != hipSuccess) return RESS_E_HIP;
     if (ress::launch_select(sp, stream) != hipSuccess) return RESS_E_HIP;
     return RESS_OK;
+}
+
+int ress_select_noalloc(const ress_shape *shape, const ress_select_params *params, const void *q, const void *k,
+                        const void *v, const float *gram, const int32_t *keep_budget, int32_t *kept_count,
+                        int32_t *kept_idx, double *drift, double *key_out, double *prob_out, hipStream_t stream)
+{
+    Grid g;
+    int st = check_shape(shape, &g);
+    if (st != RESS_OK) return st;
+    if (g.n_kb > RESS_MAX_KEY_BLOCKS) return RESS_E_UNSUPPORTED;
+    if (!params) return RESS_E_INVALID_ARG;
+    if (params->pooled_in_workspace) return RESS_E_INVALID_ARG;  // the caller cannot reach this workspace
+    if (!has_work(shape)) return RESS_OK;
+    if (workspace_bytes(shape, g) > (size_t)RESS_NOALLOC_SCRATCH_BYTES) return RESS_E_UNSUPPORTED;
+    void *ws = nullptr;
+    st = scratch_of_current_device(&ws);
+    if (st != RESS_OK) return st;
+    return ress_select(shape, params, q, k, v, gram, keep_budget, kept_count, kept_idx, drift, key_out, prob_out,
+                       ws, (size_t)RESS_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 // Shared checks of the two projections: shape, H a multiple of 4, grid size.

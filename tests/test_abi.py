@@ -27,8 +27,9 @@ def ress():
 
 def test_header_declares_the_boundary():
     assert declared_entry_points() == ["ress_dense_attn", "ress_out_proj_residual", "ress_out_proj_residual_f32",
-                                       "ress_qkv_proj_pool", "ress_select", "ress_select_workspace_size",
-                                       "ress_sparse_attn", "ress_sparse_attn_out_f32", "ress_status_string"]
+                                       "ress_qkv_proj_pool", "ress_select", "ress_select_noalloc",
+                                       "ress_select_workspace_size", "ress_sparse_attn", "ress_sparse_attn_out_f32",
+                                       "ress_status_string"]
 
 
 def test_library_exports_every_declared_symbol(ress):
