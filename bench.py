@@ -2,9 +2,12 @@
 
 One step = ress_select (pooling, drift scores, top-c, R restoration rounds,
 kept lists) + ress_sparse_attn (block-sparse attention over the kept blocks) on
-one synthetic layer whose inputs are already resident in HBM. The default
+one synthetic layer whose inputs are already resident in HBM; L2 and the
+infinity cache are flushed before every step (outside its timing). The default
 workload is 32 views x 1374 tokens (43,968 tokens), 16 heads x 64, blocks of 128,
-75% block sparsity, 5 rounds.
+75% block sparsity, 5 rounds. --config 16v_stack runs the 24-layer stack end to
+end with its float32 residual stream; --rounds-sweep adds config 3's sweep of
+the restoration rounds.
 
 Prints one JSON line (rank 0). Also reports: the dense attention baseline of the
 same library, per-kernel times from HIP events recorded on the launch stream,
@@ -39,10 +42,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="32v", help="workload: tiny, 8v, 32v, 100v, 16v_stack")
-    ap.add_argument("--sparsity", type=float, default=0.75)
+    ap.add_argument("--sparsity", type=float, default=None,
+                    help="uniform target sparsity (default: the workload's own; 100v draws per-head sparsities)")
     ap.add_argument("--bq", type=int, default=None, help="query block size (default: the workload's)")
     ap.add_argument("--bk", type=int, default=None, help="key block size (default: the workload's)")
-    ap.add_argument("--no-flush", action="store_true", help="skip the cache-flushed secondary timing")
+    ap.add_argument("--no-flush", action="store_true", help="time back-to-back steps without flushing the caches before each")
     ap.add_argument("--no-criteria", action="store_true", help="skip the per-criterion drift report")
     ap.add_argument("--no-masking", action="store_true", help="skip the single-block masking report")
     ap.add_argument("--no-neighbours", action="store_true", help="skip the fused-projection report")
@@ -52,6 +56,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for HBM counter scaling)")
+    ap.add_argument("--rounds-sweep", default=None,
+                    help="comma-separated restoration rounds: selection time and J_best/J_init per R")
     return ap.parse_args()
 
 
@@ -307,6 +313,121 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 5}))
 
 
+def timed_steps(step, n, stream, flush=None):
+    """n steps, each bracketed by HIP events on the launch stream (per-kernel
+    boundaries as recorded by `step`); with `flush`, L2 and the infinity cache are
+    overwritten before every step, outside the events. Returns [n][kernels] ms."""
+    import torch
+
+    evs = []
+    for _ in range(n):
+        if flush is not None:
+            flush()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(step.n_events)]
+        step(e)
+        evs.append(e)
+    torch.cuda.synchronize()
+    return np.array([[e[i].elapsed_time(e[i + 1]) for i in range(len(e) - 1)] for e in evs])
+
+
+def stack_run(ress, args, torch, dev, stream, flush):
+    """The 24-layer stack end to end: per layer selection + block-sparse attention
+    (timed, caches flushed before each layer), the dense attention, and the
+    change sparse attention makes to what the layer adds to the residual stream,
+    accumulated in a float32 stream of width 1024: r = sum_l W_O^l (O_sparse -
+    O_dense) against base = sum_l W_O^l O_dense (Sec. 3, "The Right Objective").
+    Layers are drawn on the host one at a time (outside the timed events)."""
+    import synth
+
+    out_layers = []
+    r = base = None
+    t_gen = 0.0
+    for layer in range(24):
+        t0 = time.time()
+        L = synth.make_config("16v_stack", layer=layer, sparsity=args.sparsity)
+        w, _ = synth.draw_w_o(L.H, L.D, L.seed)
+        w_bits = synth.f32_to_bf16_bits(w.transpose(1, 0, 2).reshape(w.shape[1], L.H * L.D).astype(np.float32))
+        q, k, v = (ress.bf16_from_bits(x, dev) for x in (L.q, L.k, L.v))
+        gram = torch.from_numpy(L.gram).to(dev)
+        w_d, w_neg = ress.bf16_from_bits(w_bits, dev), ress.bf16_from_bits(w_bits ^ np.uint16(0x8000), dev)
+        t_gen += time.time() - t0
+        if r is None:
+            r = torch.zeros((L.N, L.H * L.D), dtype=torch.float32, device=dev)
+            base = torch.zeros_like(r)
+        kc = torch.empty((L.H, L.n_qb), dtype=torch.int32, device=dev)
+        ki = torch.empty((L.H, L.n_qb, L.n_kb), dtype=torch.int32, device=dev)
+        drift = torch.empty((L.H, L.n_qb, 2), dtype=torch.float64, device=dev)
+        o_s, o_d = torch.empty_like(q), torch.empty_like(q)
+        ws = torch.empty(ress.ress_select_workspace_size(
+            ress.make_shape(L.H, L.N, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail)), dtype=torch.uint8,
+            device=dev)
+
+        def step(e=None):
+            if e is not None:
+                e[0].record(stream)
+            ress.ress_select(q, k, v, gram, L.budgets, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                             rounds=args.rounds, kept_count=kc, kept_idx=ki, drift=drift, workspace=ws, stream=stream)
+            if e is not None:
+                e[1].record(stream)
+            ress.ress_sparse_attn(q, k, v, kc, ki, bq=L.bq, bk=L.bk, out=o_s, stream=stream)
+            if e is not None:
+                e[2].record(stream)
+        step.n_events = 3
+        for _ in range(2):
+            step()
+        t = timed_steps(step, 5, stream, flush)
+        ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, out=o_d, stream=stream)
+        ress.ress_out_proj_residual_f32(o_s, w_d, r, resid_out=r, stream=stream)
+        ress.ress_out_proj_residual_f32(o_d, w_neg, r, resid_out=r, stream=stream)
+        ress.ress_out_proj_residual_f32(o_d, w_d, base, resid_out=base, stream=stream)
+        torch.cuda.synchronize()
+        dr = drift.cpu().numpy().reshape(-1, 2)
+        live = dr[:, 0] > 0
+        out_layers.append({"layer": layer, "noise_sigma": round(synth.stack_sigma(layer), 4),
+                           "select_ms": round(float(t[:, 0].mean()), 4), "sparse_attn_ms": round(float(t[:, 1].mean()), 4),
+                           "J_best_median": float(np.median(dr[live, 1])),
+                           "J_best_over_J_init_median": round(float(np.median(dr[live, 1] / dr[live, 0])), 4),
+                           "stream_drift_rel_so_far": round((torch.linalg.vector_norm(r) /
+                                                             torch.linalg.vector_norm(base)).item(), 5)})
+        del q, k, v, gram, kc, ki, drift, o_s, o_d, ws, w_d, w_neg
+    layer_ms = [x["select_ms"] + x["sparse_attn_ms"] for x in out_layers]
+    return {"layers": out_layers, "ms_per_layer_mean": round(float(np.mean(layer_ms)), 4),
+            "stack_ms": round(float(np.sum(layer_ms)), 3),
+            "stream_drift_rel": out_layers[-1]["stream_drift_rel_so_far"],
+            "host_generation_s": round(t_gen, 1)}
+
+
+def rounds_sweep(ress, L, q, k, v, gram, stream, flush, rounds_list, n=10):
+    """Config 3's sweep of the restoration rounds (the synthetic analogue of
+    Fig. 7): selection time (caches flushed before each call) and the median
+    J_best / J_init over rows that drop blocks, per R."""
+    import torch
+
+    out = []
+    for R in rounds_list:
+        drift = torch.empty((L.H, L.n_qb, 2), dtype=torch.float64, device=q.device)
+        kc = torch.empty((L.H, L.n_qb), dtype=torch.int32, device=q.device)
+        ki = torch.empty((L.H, L.n_qb, L.n_kb), dtype=torch.int32, device=q.device)
+
+        def step(e=None):
+            if e is not None:
+                e[0].record(stream)
+            ress.ress_select(q, k, v, gram, L.budgets, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                             rounds=R, kept_count=kc, kept_idx=ki, drift=drift, stream=stream)
+            if e is not None:
+                e[1].record(stream)
+        step.n_events = 2
+        step()
+        t = timed_steps(step, n, stream, flush)[:, 0]
+        dr = drift.cpu().numpy().reshape(-1, 2)
+        live = dr[:, 0] > 0
+        out.append({"rounds": R, "select_ms_mean": round(float(t.mean()), 4),
+                    "select_ms_median": round(float(np.median(t)), 4),
+                    "J_best_over_J_init_median": round(float(np.median(dr[live, 1] / dr[live, 0])), 4),
+                    "J_best_over_J_init_mean": round(float(np.mean(dr[live, 1] / dr[live, 0])), 4)})
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -324,6 +445,27 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    # Caches are flushed before every timed step by overwriting a 512 MB buffer
+    # (larger than L2 and the 256 MB infinity cache), outside the timed events.
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    flush = None if args.no_flush else (lambda: scratch.fill_(1))
+
+    if args.config == "16v_stack":
+        t0 = time.perf_counter()
+        res = stack_run(ress, args, torch, dev, stream, flush)
+        wall = time.perf_counter() - t0
+        out = {"metric": METRIC, "value": res["ms_per_layer_mean"], "unit": "ms/layer", "n_gpus": 1,
+               "steps": 5, "warmup": 2, "ms_per_step": res["ms_per_layer_mean"], "higher_is_better": False,
+               "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+               "config": {"workload": "16v_stack: 24 global-attention layers of 21,984 tokens (16 heads x 64), "
+                                      "blocks 128, noise 0.3 -> 1.0, float32 residual stream of width 1024",
+                          "sparsity_target": 0.75 if args.sparsity is None else args.sparsity,
+                          "rounds": args.rounds},
+               "stack": res, "wall_s": round(wall, 1)}
+        print(json.dumps(out), flush=True)
+        return 0
+
     t_gen = time.time()
     L = synth.make_config(args.config, sparsity=args.sparsity, bq=args.bq, bk=args.bk)
     q, k, v = (ress.bf16_from_bits(x, dev) for x in (L.q, L.k, L.v))
@@ -336,7 +478,6 @@ def main():
     o = torch.empty_like(q)
     ws = torch.empty(ress.ress_select_workspace_size(
         ress.make_shape(L.H, L.N, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail)), dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream(dev)
 
     def step(ev=None):
         if ev is not None:
@@ -348,83 +489,78 @@ def main():
         ress.ress_sparse_attn(q, k, v, kc, ki, bq=L.bq, bk=L.bk, out=o, stream=stream)
         if ev is not None:
             ev[2].record(stream)
+    step.n_events = 3
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    # Timed region: exactly `steps` steps, synchronised on both sides.
+    # Timed region: exactly `steps` steps, synchronised on both sides; each step is
+    # bracketed by HIP events on the launch stream, with the caches flushed before
+    # it (outside the events). value = mean event time of a step.
+    t0 = time.perf_counter()
+    t_flush = timed_steps(step, args.steps, stream, flush)
+    wall_incl_flush_ms = 1e3 * (time.perf_counter() - t0) / args.steps
+    sel_ms, sp_ms = t_flush[:, 0], t_flush[:, 1]
+    step_ms = sel_ms + sp_ms
+    t_sel, t_sp = float(np.mean(sel_ms)), float(np.mean(sp_ms))
+    value_ms = float(np.mean(step_ms))
+
+    # Secondary: back-to-back steps without flushing (warm L2 / infinity cache).
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    wall_ms = 1e3 * (time.perf_counter() - t0) / args.steps
+    warm_wall_ms = 1e3 * (time.perf_counter() - t0) / args.steps
+    t_warm = timed_steps(step, args.steps, stream)
+    warm = {"ms_per_step_wall": round(warm_wall_ms, 4), "select_ms_mean": round(float(t_warm[:, 0].mean()), 4),
+            "sparse_attn_ms_mean": round(float(t_warm[:, 1].mean()), 4),
+            "layer_ms_median": round(float(np.median(t_warm.sum(axis=1))), 4)}
 
-    # Per-kernel durations with events on the launch stream (separate pass).
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    for e in evs:
-        step(e)
-    torch.cuda.synchronize()
-    sel_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    sp_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
-    t_sel, t_sp = float(np.mean(sel_ms)), float(np.mean(sp_ms))
-
-    # Secondary timing with L2 and the infinity cache flushed before every step
-    # (a 512 MB buffer is overwritten outside the timed events).
-    flushed = None
-    if not args.no_flush:
-        scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-        fe = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-        for e in fe:
-            scratch.fill_(1)
-            step(e)
-        torch.cuda.synchronize()
-        f_sel = np.array([e[0].elapsed_time(e[1]) for e in fe])
-        f_sp = np.array([e[1].elapsed_time(e[2]) for e in fe])
-        f_tot = f_sel + f_sp
-        flushed = {"select_ms_median": round(float(np.median(f_sel)), 4),
-                   "sparse_attn_ms_median": round(float(np.median(f_sp)), 4),
-                   "layer_ms_median": round(float(np.median(f_tot)), 4),
-                   "layer_ms_p90": round(float(np.percentile(f_tot, 90)), 4)}
-        del scratch
-
-    # Dense baseline of the same library.
+    # Dense baseline of the same library, timed the same way (flushed).
     od = torch.empty_like(q)
-    ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, out=od, stream=stream)
-    dev_evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.dense_steps)]
-    for a, b in dev_evs:
-        a.record(stream)
-        ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, out=od, stream=stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    t_dense = float(np.mean([a.elapsed_time(b) for a, b in dev_evs]))
 
+    def dense_step(e=None):
+        if e is not None:
+            e[0].record(stream)
+        ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, out=od, stream=stream)
+        if e is not None:
+            e[1].record(stream)
+    dense_step.n_events = 2
+    dense_step()
+    t_dense = float(timed_steps(dense_step, args.dense_steps, stream, flush)[:, 0].mean())
+    t_dense_warm = float(timed_steps(dense_step, args.dense_steps, stream)[:, 0].mean())
+
+    sweep = None
+    if args.rounds_sweep:
+        sweep = rounds_sweep(ress, L, q, k, v, gram, stream, flush, [int(x) for x in args.rounds_sweep.split(",")])
     ceilings = measured_ceilings(torch, dev)
     criteria = None if args.no_criteria else criteria_report(ress, L, q, k, v, gram, od, stream)
     mask_rep = None if args.no_masking else masking_report(ress, L, q, k, v, gram, stream)
     neigh = None if args.no_neighbours else neighbours_report(ress, L, stream)
 
     kc_h, ki_h, dr = kc.cpu().numpy(), ki.cpu().numpy(), drift.cpu().numpy().reshape(-1, 2)
+    sparsity_desc = (float(L.sparsity[0]) if np.all(L.sparsity == L.sparsity[0])
+                     else f"per head in [{L.sparsity.min():.3f}, {L.sparsity.max():.3f}]")
     flops_kept, kept_tiles = kept_flops(L, kc_h, ki_h)
     flops_dense = 4.0 * L.D * L.H * float(L.N) * float(L.N)
     tf_kept = flops_kept / (t_sp * 1e-3) / 1e12
-    tf_dense_eq = flops_dense / (wall_ms * 1e-3) / 1e12
+    tf_dense_eq = flops_dense / (value_ms * 1e-3) / 1e12
     sel_bytes = select_bytes(L)
     measured_sparsity = 1.0 - kept_tiles / float(L.H * n_qb * n_kb)
     ok = dr[:, 0] > 0
     # The committed counters cover the default workload only.
-    default_workload = (args.config == "32v" and L.bq == 128 and L.bk == 128 and args.sparsity == 0.75
+    default_workload = (args.config == "32v" and L.bq == 128 and L.bk == 128 and np.all(L.sparsity == 0.75)
                         and args.rounds == 5)
     traffic = traffic_from_profile() if default_workload else None
 
     out = {
         "metric": METRIC,
-        "value": round(wall_ms, 4),
+        "value": round(value_ms, 4),
         "unit": "ms/layer",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(wall_ms, 4),
+        "ms_per_step": round(value_ms, 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -433,10 +569,12 @@ def main():
         "config": {
             "workload": f"{args.config}: one global-attention layer, {L.N} tokens "
                         f"({L.H} heads x {L.D}), blocks {L.bq}/{L.bk}, {n_qb}x{n_kb} blocks per head, "
-                        f"target sparsity {args.sparsity}, {args.rounds} restoration rounds",
+                        f"target sparsity {sparsity_desc}, {args.rounds} restoration rounds",
             "tokens": L.N, "heads": L.H, "head_dim": L.D, "block_q": L.bq, "block_k": L.bk,
-            "sparsity_target": args.sparsity,
+            "sparsity_target": sparsity_desc,
             "rounds": args.rounds, "select_dtype": "f64", "attention_dtype": "bf16 MFMA, f32 accumulate",
+            "timing": "mean of per-step HIP events, L2 and infinity cache flushed before every step"
+                      if flush is not None else "mean of per-step HIP events, back to back",
         },
         "roofline": {
             "kernel": f"attn_kernel<{L.bq},{L.bk},sparse> (ress_sparse_attn)",
@@ -447,13 +585,14 @@ def main():
             "frac": round(tf_kept / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
             "algorithmic_flops_per_launch": flops_kept,
+            "launch_ms_mean": round(t_sp, 4),
         },
         "breakdown": {
             "select_ms": round(t_sel, 4),
             "sparse_attn_ms": round(t_sp, 4),
             "selection_overhead_frac": round(t_sel / (t_sel + t_sp), 4),
             "dense_attn_ms": round(t_dense, 4),
-            "speedup_vs_dense": round(t_dense / wall_ms, 3),
+            "speedup_vs_dense": round(t_dense / value_ms, 3),
             "dense_tflops": round(flops_dense / (t_dense * 1e-3) / 1e12, 2),
             "dense_frac_peak": round(flops_dense / (t_dense * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "dense_equivalent_tflops": round(tf_dense_eq, 2),
@@ -466,11 +605,17 @@ def main():
             "select_ms_p90": round(float(np.percentile(sel_ms, 90)), 4),
             "sparse_attn_ms_median": round(float(np.median(sp_ms)), 4),
             "sparse_attn_ms_p90": round(float(np.percentile(sp_ms, 90)), 4),
+            "layer_ms_median": round(float(np.median(step_ms)), 4),
+            "layer_ms_p90": round(float(np.percentile(step_ms, 90)), 4),
+            "timed_region_wall_ms_per_step_incl_flush": round(wall_incl_flush_ms, 4),
+            "warm_cache": warm,
+            "dense_attn_ms_warm": round(t_dense_warm, 4),
+            "speedup_vs_dense_warm": round(t_dense_warm / warm["layer_ms_median"], 3),
             "kept_only_frac_of_measured_gemm": round(tf_kept / ceilings["bf16_gemm_8192_tflops"], 4),
             "select_frac_of_measured_copy": round(sel_bytes / (t_sel * 1e-3) / 1e9 /
                                                   ceilings["copy_1gib_read_plus_write_gbs"], 4),
             "measured_ceilings": ceilings,
-            "cache_flushed": flushed,
+            "rounds_sweep": sweep,
             "criteria_same_budget": criteria,
             "single_block_masking": mask_rep,
             "fused_neighbours": neigh,
@@ -479,7 +624,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, args.rounds, kc_h, ki_h, args.cpu_seconds)
-        out["cpu_baseline"]["gpu_speedup"] = round(out["cpu_baseline"]["value"] / wall_ms, 1)
+        out["cpu_baseline"]["gpu_speedup"] = round(out["cpu_baseline"]["value"] / value_ms, 1)
     print(json.dumps(out), flush=True)
     return 0
 
