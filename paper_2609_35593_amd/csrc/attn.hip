@@ -39,9 +39,10 @@
 // logits are formed exactly; either way every score of a row has one form.
 // Softmax is invariant to the reference, so this changes rounding only.
 //
-// Workgroups are numbered so that the 8 XCDs each receive a contiguous range of
-// (head, query block) items: neighbouring query blocks of a head share an XCD
-// and its L2, where their K/V tiles are re-read.
+// Workgroups are numbered so that each of the 8 XCDs runs a contiguous chunk of
+// query blocks of every head: neighbouring query blocks of a head share an XCD
+// and its L2, where their K/V tiles are re-read, and heads of different cost
+// (ragged budgets) are spread evenly over the XCDs.
 #include <type_traits>
 
 #include "ress_internal.h"
@@ -91,11 +92,19 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
     __shared__ __attribute__((aligned(1024))) unsigned char v_lds0[TILE];
     __shared__ __attribute__((aligned(1024))) unsigned char v_lds1[TILE];
 
+    // Work order: XCD x runs, head after head, one eighth of every head's query
+    // blocks (a contiguous chunk, so neighbouring query blocks share the XCD's L2),
+    // the chunk rotating with the head so that every XCD gets the same mix of heads
+    // (ragged per-head budgets stay balanced across XCDs) and the dense tail chunks
+    // of different heads land on different XCDs. Within a head, last blocks first.
     const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-    const int item = xcd * p.items_per_xcd + local;
-    if (item >= p.H * p.n_qb) return;
-    const int h = item / p.n_qb;
-    const int i = p.n_qb - 1 - item % p.n_qb;  // last query blocks first (they may be dense)
+    const int chunk = p.qb_chunk;
+    const int slot = local / chunk, r = local - slot * chunk;
+    if (slot >= p.H) return;
+    const int h = (xcd + slot) % p.H;
+    const int i_fwd = ((xcd - h % 8 + 8) & 7) * chunk + r;
+    if (i_fwd >= p.n_qb) return;
+    const int i = p.n_qb - 1 - i_fwd;
     const int N = p.N, n_kb = p.n_kb;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -467,7 +476,7 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
 template <int BQ, int BK>
 hipError_t launch_bk(const AttnParams &p, bool sparse, hipStream_t s)
 {
-    const dim3 grid((unsigned)(8 * p.items_per_xcd)), block(BQ * 2);
+    const dim3 grid((unsigned)(8 * p.H * p.qb_chunk)), block(BQ * 2);
     if (sparse)
         hipLaunchKernelGGL((attn_kernel<BQ, BK, true>), grid, block, 0, s, p);
     else

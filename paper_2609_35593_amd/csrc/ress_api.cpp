@@ -322,15 +322,14 @@ static int attn_common(const ress_shape *shape, const void *q, const void *k, co
     if (o == q || o == k || o == v) return RESS_E_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return RESS_E_INVALID_ARG;
     if (sparse && (!kept_count || !kept_idx)) return RESS_E_INVALID_ARG;
-    const long long items = (long long)shape->H * g.n_qb;
-    const long long per_xcd = (items + 7) / 8;
-    if (8 * per_xcd > 0x7fffffffLL) return RESS_E_UNSUPPORTED;
+    const long long chunk = (g.n_qb + 7) / 8;
+    if (8 * chunk * shape->H > 0x7fffffffLL) return RESS_E_UNSUPPORTED;
     ress::AttnParams ap;
     ap.H = shape->H;
     ap.N = shape->N;
     ap.n_qb = (int)g.n_qb;
     ap.n_kb = (int)g.n_kb;
-    ap.items_per_xcd = (int)per_xcd;
+    ap.qb_chunk = (int)chunk;
     ap.scale_log2 = scale * 1.4426950408889634f;
     ap.q = static_cast<const uint16_t *>(q);
     ap.k = static_cast<const uint16_t *>(k);

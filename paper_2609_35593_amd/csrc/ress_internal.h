@@ -46,7 +46,7 @@ struct SelectParams {
 
 struct AttnParams {
     int H, N, n_qb, n_kb;
-    int items_per_xcd;  // work items assigned to each of the 8 XCDs
+    int qb_chunk;       // query blocks per (head, XCD): ceil(n_qb / 8)
     float scale_log2;   // softmax scale * log2(e)
     const uint16_t *q, *k, *v;
     uint16_t *o;                           // bf16 output, unless o32 is set
