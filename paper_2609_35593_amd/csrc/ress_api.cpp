@@ -39,28 +39,38 @@ bool has_work(const ress_shape *s) { return s->H > 0 && s->N > 0; }
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 bool aligned16(const void *ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 
-// Workspace: qbar [H][n_qb][64], then kbarT, vbar, vbarT, each [H][n_kb][64], then
-// cT [H][n_kb] (float64), every region 256-byte aligned.
+// Workspace: qbar [H][n_qb][64], kbarT [H][64][ks], vbar [H][n_kb][64], vbarT
+// [H][64][ks], cT [H][n_kb] (float64, ks = n_kb rounded up to even), every
+// region 256-byte aligned.
+struct Regions {
+    size_t qb, kt, vb, cb;
+};
+
+Regions regions(const ress_shape *s, const Grid &g)
+{
+    const size_t ks = (size_t)ress::pooled_kstride((int)g.n_kb);
+    return {align256((size_t)s->H * g.n_qb * kD * sizeof(double)), align256((size_t)s->H * kD * ks * sizeof(double)),
+            align256((size_t)s->H * g.n_kb * kD * sizeof(double)), align256((size_t)s->H * g.n_kb * sizeof(double))};
+}
+
 size_t workspace_bytes(const ress_shape *s, const Grid &g)
 {
-    const size_t qb = align256((size_t)s->H * g.n_qb * kD * sizeof(double));
-    const size_t kb = align256((size_t)s->H * g.n_kb * kD * sizeof(double));
-    const size_t cb = align256((size_t)s->H * g.n_kb * sizeof(double));
-    return qb + 3 * kb + cb;
+    const Regions r = regions(s, g);
+    return r.qb + 2 * r.kt + r.vb + r.cb;
 }
 
 // Pooled state inside the workspace (the regions workspace_bytes sizes).
 ress::Pooled pooled_layout(const ress_shape *s, const Grid &g, void *workspace)
 {
     char *w = static_cast<char *>(workspace);
-    const size_t qb = align256((size_t)s->H * g.n_qb * kD * sizeof(double));
-    const size_t kb = align256((size_t)s->H * g.n_kb * kD * sizeof(double));
+    const Regions r = regions(s, g);
     ress::Pooled pooled;
     pooled.qbar = reinterpret_cast<double *>(w);
-    pooled.kbarT = reinterpret_cast<double *>(w + qb);
-    pooled.vbar = reinterpret_cast<double *>(w + qb + kb);
-    pooled.vbarT = reinterpret_cast<double *>(w + qb + 2 * kb);
-    pooled.cT = reinterpret_cast<double *>(w + qb + 3 * kb);
+    pooled.kbarT = reinterpret_cast<double *>(w + r.qb);
+    pooled.vbar = reinterpret_cast<double *>(w + r.qb + r.kt);
+    pooled.vbarT = reinterpret_cast<double *>(w + r.qb + r.kt + r.vb);
+    pooled.cT = reinterpret_cast<double *>(w + r.qb + 2 * r.kt + r.vb);
+    pooled.kstride = ress::pooled_kstride((int)g.n_kb);
     return pooled;
 }
 

@@ -13,13 +13,18 @@ constexpr int kD = 64;      // head dimension handled by every kernel
 constexpr int kWave = 64;   // CDNA wavefront width
 
 // Pooled tensors of one layer, float64, carved out of the selection workspace.
+// The channel-major tensors have rows of kstride = n_kb rounded up to even, so
+// that every run of whole rows starts on a 16-byte boundary.
 struct Pooled {
-    double *qbar;   // [H][n_qb][64]   query block means
-    double *kbarT;  // [H][64][n_kb]   key block means, channel-major
-    double *vbar;   // [H][n_kb][64]   value block means
-    double *vbarT;  // [H][64][n_kb]   value block means, channel-major
-    double *cT;     // [H][n_kb]       Vbar_j^T M_h Vbar_j
+    double *qbar;   // [H][n_qb][64]       query block means
+    double *kbarT;  // [H][64][kstride]    key block means, channel-major
+    double *vbar;   // [H][n_kb][64]       value block means
+    double *vbarT;  // [H][64][kstride]    value block means, channel-major
+    double *cT;     // [H][n_kb]           Vbar_j^T M_h Vbar_j
+    int kstride;
 };
+
+__host__ __device__ inline int pooled_kstride(int n_kb) { return (n_kb + 1) & ~1; }
 
 struct PoolParams {
     int H, N, bq, bk, n_qb, n_kb;

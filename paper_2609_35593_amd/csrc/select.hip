@@ -2,15 +2,25 @@
 // layer: pooled map, drift scores, exact top-c, R budget-neutral restoration
 // rounds with track-best, and compaction of the kept-block lists.
 //
-// Work layout. A workgroup holds 4 independent waves; each wave owns R query
-// blocks ("rows") of one head, so every load of the head's pooled key/value
-// tensors is used by the R rows in registers and by the 4 waves through L1.
+// Work layout. A workgroup of NW waves owns NW x R query blocks ("rows") of one
+// head; each wave owns R of them.
 //  - Per-candidate quantities live "lane <-> key block": lane l, slot c holds key
-//    block j = l + 64 c (CPL slots).
-//  - Per-row vectors (Qbar, vbar, S vbar with S the symmetric part of M, g, M g)
-//    live "lane <-> channel"
-//    (D = 64 is the wave width) and are broadcast to the candidate lanes through
-//    the wave's LDS area, two doubles per read.
+//    block j = l + 64 c (CPL slots). Per-row vectors (Qbar, vbar, S vbar with S
+//    the symmetric part of M, g, M g) live in the wave's LDS area, channel d at
+//    index d, and are read as broadcasts.
+//  - Every pass over the head's pooled tensors (the pooled logits against
+//    Kbar, then the dense pooled output, the drift scores, the net drift and
+//    every round's gains against Vbar) streams the channel-major tensor through
+//    LDS once per workgroup: stages of SC channel rows move global -> LDS by DMA
+//    (global_load_lds, 1 KB per wave instruction, no registers held) into a ring
+//    of 3 to 6 slots, each stage issued as far ahead of its use as the ring
+//    allows, with one workgroup barrier per stage;
+//    each wave then reads its key blocks of every channel row from LDS (64
+//    consecutive doubles per read: no bank conflicts). All rows of the
+//    workgroup share every stage, so the tensors cross L2 once per NW x R rows.
+//  - The weighted sums over key blocks (vbar = sum_j P_j Vbar_j, g = sum over the
+//    drop set) are formed per lane over its slots and combined across the wave
+//    by a butterfly that halves the channels each lane carries at every step.
 //  - Every top-k is exact: a bitwise search for the k-th largest of
 //    order-preserving 64-bit keys, using wave ballots and popcounts, ties broken
 //    by the lower block index. No atomics and no data-dependent reduction
@@ -24,20 +34,54 @@
 namespace ress {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
+typedef __attribute__((address_space(3))) void lds_void;
+
 // Word 3 of a raw buffer descriptor on gfx9-family chips (32-bit data format,
 // no swizzle, no index stride): loads past num_records bytes return zero.
 constexpr int kBufWord3 = 0x00020000;
 
-// Buffer descriptor over one head's pooled tensor (n_kb x 64 doubles, either layout).
+// Channel rows per stage: the most (a power of two up to 8) whose stage of
+// 64 CPL key blocks fits 36 KB; one row (up to 32 KB) for the largest rows.
+// Larger stages keep more bytes in flight per barrier (the passes over long
+// rows are bound by the DMA round trip, not by arithmetic).
+template <int CPL>
+constexpr int kSC = (CPL * 512 * 8 <= 36864) ? 8 : (CPL * 512 * 4 <= 36864) ? 4 : (CPL * 512 * 2 <= 36864) ? 2 : 1;
+template <int SC>
+constexpr int kLog2 = SC == 8 ? 3 : SC == 4 ? 2 : SC == 2 ? 1 : 0;
+// Bytes of one ring slot, and the number of slots: as many as the LDS left by
+// the wave areas and M_h holds, from 3 up to 6 (each stage is issued slots - 1
+// stages ahead of its use).
+template <int CPL>
+constexpr int kSlotBytes = (CPL * 512 * kSC<CPL> + 1023) / 1024 * 1024;
+template <int CPL, int OTHER>
+constexpr int kNBuf = ((163840 - OTHER) / kSlotBytes<CPL>) > 6 ? 6 : ((163840 - OTHER) / kSlotBytes<CPL>);
+
+// Wait until at most n (0..63) of this wave's vector memory operations are
+// outstanding (loads complete in issue order: everything older than the last n
+// has landed). The count is an immediate of s_waitcnt, hence the dispatch.
+template <int N>
+__device__ __forceinline__ void wait_vm_dispatch(int n)
+{
+    if constexpr (N < 64) {
+        if (n == N) {
+            __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+            return;
+        }
+        wait_vm_dispatch<N + 1>(n);
+    } else {
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // out of range: wait for everything
+    }
+}
+__device__ __forceinline__ void wait_vm(int n) { wait_vm_dispatch<0>(n); }
+
+// Buffer descriptor over one head's row-major pooled Vbar (n_kb x 64 doubles).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t pooled_rsrc(const double *base, int nkb)
 {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<double *>(base), 0, kD * nkb * (int)sizeof(double),
                                              kBufWord3);
 }
 
-// Channel `lane` of row j (wave-uniform) of a row-major pooled tensor.
+// Channel `lane` of row j (wave-uniform) of the row-major pooled Vbar.
 __device__ __forceinline__ double pooled_row(__amdgpu_buffer_rsrc_t rs, int j, int lane)
 {
     return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(
@@ -59,6 +103,40 @@ __device__ __forceinline__ double wave_max(double x)
     return x;
 }
 
+// Sum over the wave of N per-lane values v[0..N-1] (channel dd of a stage):
+// log2(N) exchange steps each keep half of the channels (the lane with the mask
+// bit set keeps the upper half and receives its partner's upper half), then a
+// plain butterfly over the remaining lanes. Lane l returns the total of channel
+// l >> (6 - log2 N); fixed order, identical across the lanes sharing it. Every
+// index is a compile-time constant (the values stay in registers).
+template <int N, int M>
+__device__ __forceinline__ double channel_sums_step(const double (&v)[N], int lane)
+{
+    if constexpr (N == 1) {
+        double x = v[0];
+#pragma unroll
+        for (int m = M; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+        return x;
+    } else {
+        constexpr int H = N / 2;
+        const bool hi = (lane & M) != 0;
+        double w[H];
+#pragma unroll
+        for (int i = 0; i < H; ++i) {
+            const double send = hi ? v[i] : v[H + i];
+            const double keep = hi ? v[H + i] : v[i];
+            w[i] = keep + __shfl_xor(send, M);
+        }
+        return channel_sums_step<H, M / 2>(w, lane);
+    }
+}
+
+template <int SC>
+__device__ __forceinline__ double channel_sums(const double (&v)[SC], int lane)
+{
+    return channel_sums_step<SC, 32>(v, lane);
+}
+
 // Order-preserving map of a double to uint64 (larger value -> larger key);
 // -0 is folded onto +0 so that equal values get equal keys.
 __device__ __forceinline__ unsigned long long order_key(double x)
@@ -67,22 +145,26 @@ __device__ __forceinline__ unsigned long long order_key(double x)
     return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-// Exact top-k of the member slots by (key desc, block index asc). memb[c] is the
-// wave-wide mask of member lanes of slot c. Returns this lane's chosen slots as
-// a bit mask. Requires 0 <= k <= number of members.
+// Exact top-k of the member slots by (key desc, block index asc). Bit c of
+// mbits marks this lane's slot c as a member. Non-member keys are replaced by 0,
+// below every member key (an order key of a finite value is at least 1), so one
+// ballot per slot counts members only. Returns this lane's chosen slots as a
+// bit mask. Requires 0 <= k <= number of members.
 template <int CPL>
-__device__ unsigned long long topk_slots(const unsigned long long (&key)[CPL],
-                                         const unsigned long long (&memb)[CPL], int k,
-                                         unsigned long long lane_bit, unsigned long long lane_lt)
+__device__ __forceinline__ unsigned long long topk_slots(const unsigned long long (&key)[CPL],
+                                                         unsigned long long mbits, int k, unsigned long long lane_lt)
 {
     if (k <= 0) return 0ull;
+    unsigned long long km[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) km[c] = ((mbits >> c) & 1ull) ? key[c] : 0ull;
     unsigned long long thr = 0;  // invariant: #members with key >= thr is >= k
     bool exact = false;
     for (int b = 63; b >= 0; --b) {
         const unsigned long long cand = thr | (1ull << b);
         int cnt = 0;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) cnt += __popcll(__ballot(key[c] >= cand) & memb[c]);
+        for (int c = 0; c < CPL; ++c) cnt += __popcll(__ballot(km[c] >= cand));
         if (cnt >= k) {
             thr = cand;
             if (cnt == k) {  // exactly k keys reach thr: they are the top k
@@ -95,23 +177,73 @@ __device__ unsigned long long topk_slots(const unsigned long long (&key)[CPL],
     if (exact) {
 #pragma unroll
         for (int c = 0; c < CPL; ++c)
-            if ((memb[c] & lane_bit) && key[c] >= thr) chosen |= 1ull << c;
+            if (km[c] >= thr) chosen |= 1ull << c;
         return chosen;
     }
     // thr is the k-th largest key; take all larger ones and the lowest-index ties.
     int gt = 0;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) gt += __popcll(__ballot(key[c] > thr) & memb[c]);
+    for (int c = 0; c < CPL; ++c) gt += __popcll(__ballot(km[c] > thr));
     const int need = k - gt;
     int before = 0;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
-        const unsigned long long tb = __ballot(key[c] == thr) & memb[c];
+        const bool tie = km[c] == thr;
+        const unsigned long long tb = __ballot(tie);
         const int rank = before + __popcll(tb & lane_lt);
-        if ((memb[c] & lane_bit) && (key[c] > thr || ((tb & lane_bit) && rank < need))) chosen |= 1ull << c;
+        if (km[c] > thr || (tie && rank < need)) chosen |= 1ull << c;
         before += __popcll(tb);
     }
     return chosen;
+}
+
+// The same selection as topk_slots for small k, by k extractions of the largest
+// remaining member key: per lane the largest over its slots (lowest slot on
+// ties), then over the wave (a butterfly), then the lowest block index among
+// the slots holding that key (slots in ascending order, lanes in ascending
+// order within a slot, which is ascending block index).
+template <int CPL>
+__device__ __forceinline__ unsigned long long topk_small(const unsigned long long (&key)[CPL],
+                                                         unsigned long long mbits, int k, int lane)
+{
+    unsigned long long left = mbits, chosen = 0;
+    for (int t = 0; t < k; ++t) {
+        unsigned long long best = 0;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const unsigned long long v = ((left >> c) & 1ull) ? key[c] : 0ull;
+            best = v > best ? v : best;
+        }
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const unsigned long long other = __shfl_xor(best, o);
+            best = other > best ? other : best;
+        }
+        // best > 0: at least one member is left (k <= members)
+        bool done = false;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const unsigned long long at = __ballot(((left >> c) & 1ull) && key[c] == best);
+            if (!done && at != 0ull) {
+                if (lane == __builtin_ctzll(at)) {
+                    left &= ~(1ull << c);
+                    chosen |= 1ull << c;
+                }
+                done = true;
+            }
+        }
+    }
+    return chosen;
+}
+
+// Top-k of the member slots: extraction for k up to 2, bitwise search beyond
+// (measured: extraction costs more than the search from k = 5 on).
+template <int CPL>
+__device__ __forceinline__ unsigned long long topk_any(const unsigned long long (&key)[CPL],
+                                                       unsigned long long mbits, int k, int lane,
+                                                       unsigned long long lane_lt)
+{
+    return k <= 2 ? topk_small<CPL>(key, mbits, k, lane) : topk_slots<CPL>(key, mbits, k, lane_lt);
 }
 
 // Swap count of round r (Eq. 17): max(floor, floor(rho c 2^-(r+1))).
@@ -121,20 +253,19 @@ __device__ __forceinline__ int swaps_of_round(int c, double rho, int r, int swap
     return m > swap_floor ? m : swap_floor;
 }
 
-// Per-wave LDS area (doubles): broadcast vectors vec[slot][R][64], one slot of
-// block weights wts[R][64], and a swap list of up to 64 (block, weight) pairs plus
-// padding to a multiple of 8. Every part starts on a 16-byte boundary.
+// Per-wave LDS area (doubles): vectors vec[slot][R][64] and a swap list of up to
+// 64 (block, weight) pairs plus padding to a multiple of 8. Every part starts on
+// a 16-byte boundary.
 template <int R>
 struct WaveLds {
-    static constexpr int kVecs = 3;  // 0: Qbar then vbar, 1: M vbar then M g, 2: g
+    static constexpr int kVecs = 3;  // 0: Qbar then vbar, 1: S vbar then M g, 2: g
     static constexpr int kSwaps = 72;
-    static constexpr int kDoubles = kVecs * R * kD + R * 64 + kSwaps + kSwaps / 2;
+    static constexpr int kDoubles = kVecs * R * kD + kSwaps + kSwaps / 2;
     static_assert(kDoubles % 2 == 0, "16-byte aligned wave areas");
     double *base;
     __device__ double *vec(int slot, int r) const { return base + (slot * R + r) * kD; }
-    __device__ double *wts(int r) const { return base + kVecs * R * kD + r * 64; }
-    __device__ double *swap_w() const { return base + kVecs * R * kD + R * 64; }
-    __device__ int *swap_j() const { return reinterpret_cast<int *>(base + kVecs * R * kD + R * 64 + kSwaps); }
+    __device__ double *swap_w() const { return base + kVecs * R * kD; }
+    __device__ int *swap_j() const { return reinterpret_cast<int *>(base + kVecs * R * kD + kSwaps); }
 };
 
 // x_r = M y_r for the R rows, lane <-> output channel, M row-major in LDS (padded
@@ -161,150 +292,69 @@ __device__ __forceinline__ void mat_vec(const float *Ms, double *const (&y)[R], 
     }
 }
 
-// Pass over the head's key blocks, lane <-> channel, with per-row block weights
-// w_r(j) held by the lane owning block j (slot c):
-//   SUB: out_r = sum_j w_r(j) (x_r - Vbar_j)      (net drift g, Eq. 10)
-//  !SUB: out_r = sum_j w_r(j) Vbar_j              (dense pooled output, Eq. 1)
-// in ascending block order with eight rows of Vbar in flight; the weights of one
-// slot (64 blocks) at a time are staged in the wave's LDS area.
-template <int CPL, int R, bool SUB>
-__device__ __forceinline__ void block_pass(const WaveLds<R> &lds, const double (&w)[R][CPL], const double (&x)[R],
-                                           const double *__restrict__ Vr, int nkb, int lane, double (&out)[R])
+template <int CPL, int R, int NW>
+__global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p)
 {
-    const __amdgpu_buffer_rsrc_t rsV = pooled_rsrc(Vr, nkb);
-#pragma unroll
-    for (int r = 0; r < R; ++r) out[r] = 0.0;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-        __builtin_amdgcn_wave_barrier();
-#pragma unroll
-        for (int r = 0; r < R; ++r) lds.wts(r)[lane] = w[r][c];  // 0 past the last block
-        __builtin_amdgcn_wave_barrier();
-        const int lim = min(64, nkb - 64 * c);
-        for (int l0 = 0; l0 < lim; l0 += 8) {
-            double vj[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) vj[u] = pooled_row(rsV, 64 * c + min(l0 + u, lim - 1), lane);
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const double *wr = lds.wts(r) + l0;
-#pragma unroll
-                for (int u = 0; u < 8; u += 2) {
-                    const double2 pw = *reinterpret_cast<const double2 *>(wr + u);
-                    if (SUB)
-                        out[r] = fma(pw.y, x[r] - vj[u + 1], fma(pw.x, x[r] - vj[u], out[r]));
-                    else
-                        out[r] = fma(pw.y, vj[u + 1], fma(pw.x, vj[u], out[r]));
-                }
-            }
-        }
-    }
-    __builtin_amdgcn_wave_barrier();
-}
-
-// Per-shape tuning, measured: the 32-view shape (6 slots, 2 rows) runs faster with
-// three workgroups per CU (168 VGPRs); 17+ slots run faster with fewer channel
-// loads unrolled (fewer registers held by loads in flight).
-template <int CPL, int R>
-constexpr int kMinBlocks = (CPL == 6 && R == 2) ? 3 : 1;
-template <int CPL>
-constexpr int kUnroll = CPL >= 17 ? 2 : 4;
-
-// acc[r][c] = sum_d T[d][jc[c]] * x_r[d] over the 64 channels of a channel-major
-// pooled tensor T (lane <-> key block), in ascending d with the same fused
-// multiply-adds whichever loop order is used. SUB: sum_d (y_r[d] - T[d][jc[c]]) x_r[d].
-// Few slots and rows: channels outermost, so the loads of every slot are in flight
-// together; otherwise slots outermost (fewer registers held by loads; measured:
-// the channel-outer order costs the 4-slot, 4-row shape its second wave per SIMD).
-template <int CPL, int R, bool SUB>
-__device__ __forceinline__ void column_dots(const double *__restrict__ T, const int (&jc)[CPL], int nkb,
-                                            double *const (&x)[R], double *const (&y)[R], double (&acc)[R][CPL])
-{
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
-    // Buffer loads: a per-lane 32-bit byte offset (the key block) and a wave-uniform
-    // one (the channel row), range-checked by the hardware against the head's tensor.
-    const __amdgpu_buffer_rsrc_t rs = pooled_rsrc(T, nkb);
-    unsigned off[CPL];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) off[c] = (unsigned)jc[c] * (unsigned)sizeof(double);
-    const int stride = nkb * (int)sizeof(double);
-    auto at = [&](int d, int c) __attribute__((always_inline)) {
-        return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(rs, off[c], d * stride, 0));
-    };
-    if constexpr (CPL <= 8 && CPL * R <= 12) {
-#pragma unroll 1
-        for (int d = 0; d < kD; d += 2) {
-            double t0[CPL], t1[CPL];
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                t0[c] = at(d, c);
-                t1[c] = at(d + 1, c);
-            }
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const double2 xd = *reinterpret_cast<const double2 *>(x[r] + d);
-                double2 yd = {0.0, 0.0};
-                if (SUB) yd = *reinterpret_cast<const double2 *>(y[r] + d);
-#pragma unroll
-                for (int c = 0; c < CPL; ++c) {
-                    if (SUB)
-                        acc[r][c] = fma(yd.y - t1[c], xd.y, fma(yd.x - t0[c], xd.x, acc[r][c]));
-                    else
-                        acc[r][c] = fma(xd.y, t1[c], fma(xd.x, t0[c], acc[r][c]));
-                }
-            }
-        }
-    } else {
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-#pragma unroll kUnroll<CPL>
-            for (int d = 0; d < kD; d += 2) {
-                const double t0 = at(d, c), t1 = at(d + 1, c);
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const double2 xd = *reinterpret_cast<const double2 *>(x[r] + d);
-                    if (SUB) {
-                        const double2 yd = *reinterpret_cast<const double2 *>(y[r] + d);
-                        acc[r][c] = fma(yd.y - t1, xd.y, fma(yd.x - t0, xd.x, acc[r][c]));
-                    } else {
-                        acc[r][c] = fma(xd.y, t1, fma(xd.x, t0, acc[r][c]));
-                    }
-                }
-            }
-        }
-    }
-}
-
-template <int CPL, int R, bool CDF>
-__global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(const SelectParams p)
-{
-    __shared__ __align__(16) double smem[kWaves * WaveLds<R>::kDoubles];
+    constexpr int SC = kSC<CPL>;                           // channel rows per stage
+    constexpr int NS = kD / SC;                            // stages per pass
+    constexpr int SB = kSlotBytes<CPL>;                    // bytes per ring slot
+    constexpr int OTHER = NW * WaveLds<R>::kDoubles * 8 + kD * (kD + 1) * 4 + 2048;
+    constexpr int NB = kNBuf<CPL, OTHER>;                  // ring slots
+    static_assert(NB >= 3, "at least three ring slots");
+    __shared__ __attribute__((aligned(1024))) unsigned char ring[NB * SB];
+    __shared__ __align__(16) double wareas[NW * WaveLds<R>::kDoubles];
     __shared__ float Ms[kD * (kD + 1)];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const unsigned long long lane_bit = 1ull << lane, lane_lt = lane_bit - 1ull;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const unsigned long long lane_lt = (1ull << lane) - 1ull;
     // Workgroups are numbered so that each of the 8 XCDs gets a contiguous range
     // of (head, row group) items: the rows of a head share one XCD's L2.
-    const int groups = (p.n_qb + kWaves * R - 1) / (kWaves * R);
+    const int groups = (p.n_qb + NW * R - 1) / (NW * R);
     const int item = (blockIdx.x & 7) * p.items_per_xcd + (blockIdx.x >> 3);
-    if (item >= p.H * groups) return;
+    if (item >= p.H * groups) return;  // the whole workgroup
     const int h = item / groups;
-    const int row0 = (item % groups) * kWaves * R + wave * R;
+    const int row0 = (item % groups) * NW * R + wave * R;
+    const int nkb = p.n_kb, nqb = p.n_qb, ks = p.pooled.kstride;
+
+    // Stage k of the workgroup's sequence holds channel rows (k mod NS) SC ..
+    // +SC-1 of Kbar^T for the first pass and of Vbar^T for every later one. Each
+    // wave issues its share of the stage's 1 KB DMA instructions; lanes past the
+    // stage's end re-read its last 16 bytes (in bounds) into the slot's slack.
+    const unsigned char *Kt = reinterpret_cast<const unsigned char *>(p.pooled.kbarT + (size_t)h * kD * ks);
+    const unsigned char *Vt = reinterpret_cast<const unsigned char *>(p.pooled.vbarT + (size_t)h * kD * ks);
+    const int sbytes = SC * ks * (int)sizeof(double);
+    const int ninstr = (sbytes + 1023) >> 10;
+    const int mine = (ninstr - wave + NW - 1) / NW;  // this wave's DMA instructions per stage
+    auto issue = [&](int k) __attribute__((always_inline)) {
+        const unsigned char *src = (k < NS ? Kt : Vt) + (size_t)(k % NS) * sbytes;
+        unsigned char *dst = ring + (k % NB) * SB;
+        for (int u = wave; u < ninstr; u += NW) {
+            const int off = min(u * 1024 + lane * 16, sbytes - 16);
+            __builtin_amdgcn_global_load_lds((const void *)(src + off), (lds_void *)(dst + u * 1024), 16, 0, 0);
+        }
+    };
+    int kc = 0;  // next stage to consume
+    for (int k = 0; k < NB - 1; ++k) issue(k);
     {
         const float *Mh = p.gram + (size_t)h * kD * kD;
-        for (int e = tid; e < kD * kD; e += kThreads) Ms[(e >> 6) * (kD + 1) + (e & 63)] = Mh[e];
+        for (int e = tid; e < kD * kD; e += NW * 64) Ms[(e >> 6) * (kD + 1) + (e & 63)] = Mh[e];
     }
-    __syncthreads();
-    if (row0 >= p.n_qb) return;  // waves are independent from here on
-    const WaveLds<R> lds{smem + wave * WaveLds<R>::kDoubles};
+    // Stage kc is ready for every wave once this wave's DMAs older than the
+    // NB - 2 stages issued after it have landed and the workgroup has met (which
+    // also frees the slot of stage kc + NB - 1, last read as stage kc - 1); then
+    // stage kc + NB - 1 is issued.
+    auto next_stage = [&]() __attribute__((always_inline)) -> const double * {
+        wait_vm((NB - 2) * mine);
+        __syncthreads();
+        issue(kc + NB - 1);
+        const double *T = reinterpret_cast<const double *>(ring + (kc % NB) * SB);
+        ++kc;
+        return T;
+    };
 
-    const int nkb = p.n_kb, nqb = p.n_qb;
+    const WaveLds<R> lds{wareas + wave * WaveLds<R>::kDoubles};
     const double eps = p.eps;
-    const double *Kt = p.pooled.kbarT + (size_t)h * kD * nkb;
     const double *Vr = p.pooled.vbar + (size_t)h * nkb * kD;
-    const double *Vt = p.pooled.vbarT + (size_t)h * kD * nkb;
     const double *cT = p.pooled.cT + (size_t)h * nkb;
     const int c_h = p.budgets[h];
     const int n_p = p.first_forced;  // candidates are the key blocks j < first_forced
@@ -322,21 +372,109 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
         gv[r] = lds.vec(2, r);
         vbv[r][lane] = p.pooled.qbar[((size_t)h * nqb + irow[r]) * kD + lane];  // Qbar_i for now
     }
-    int jc[CPL];  // this lane's key block per slot, clamped into range for loads
+    int jc[CPL];  // this lane's key block per slot, clamped into range for reads
     bool valid[CPL];
-    unsigned long long memb[CPL];  // wave masks of candidate lanes per slot
+    unsigned long long cand_bits = 0;  // bit c: slot c of this lane is a candidate
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
         const int j = lane + 64 * c;
         valid[c] = j < nkb;
         jc[c] = valid[c] ? j : nkb - 1;
-        memb[c] = __ballot(j < n_p);
+        if (j < n_p) cand_bits |= 1ull << c;
     }
     __builtin_amdgcn_wave_barrier();
 
+    // acc[r][c] = sum_d x_r[d] T[d][j_c], or with SUB sum_d (y_r[d] - T[d][j_c]) x_r[d],
+    // in ascending d, over one pass of the ring.
+    auto dot_pass = [&](auto sub, double *const (&x)[R], double *const (&y)[R],
+                        double (&acc)[R][CPL]) __attribute__((always_inline)) {
+        constexpr bool SUB = decltype(sub)::value;
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
+        for (int s = 0; s < NS; ++s) {
+            const double *T = next_stage();
+            if constexpr (SC == 1) {
+                double xd[R], yd[R];
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    xd[r] = x[r][s];
+                    yd[r] = SUB ? y[r][s] : 0.0;
+                }
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    const double t = T[jc[c]];
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+                        acc[r][c] = SUB ? fma(yd[r] - t, xd[r], acc[r][c]) : fma(xd[r], t, acc[r][c]);
+                }
+            } else {
+                // Channel pairs one at a time (registers for two waves per SIMD or more).
+#pragma unroll 1
+                for (int dd = 0; dd < SC; dd += 2) {
+                    const int d = s * SC + dd;
+                    double2 xd[R], yd[R];
+#pragma unroll
+                    for (int r = 0; r < R; ++r) {
+                        xd[r] = *reinterpret_cast<const double2 *>(x[r] + d);
+                        if (SUB) yd[r] = *reinterpret_cast<const double2 *>(y[r] + d);
+                    }
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c) {
+                        const double t0 = T[dd * ks + jc[c]], t1 = T[(dd + 1) * ks + jc[c]];
+#pragma unroll
+                        for (int r = 0; r < R; ++r) {
+                            if (SUB)
+                                acc[r][c] = fma(yd[r].y - t1, xd[r].y, fma(yd[r].x - t0, xd[r].x, acc[r][c]));
+                            else
+                                acc[r][c] = fma(xd[r].y, t1, fma(xd[r].x, t0, acc[r][c]));
+                        }
+                    }
+                }
+            }
+        }
+    };
+    // out_r[d] = sum_j w_r(j) T[d][j], or with SUB sum_j w_r(j) (y_r[d] - T[d][j]),
+    // for every channel d, into the wave's LDS vector out_r: per lane over its
+    // slots in ascending order, then across the wave (channel_sums).
+    auto wsum_pass = [&](auto sub, const double (&w)[R][CPL], double *const (&y)[R],
+                         double *const (&out)[R]) __attribute__((always_inline)) {
+        constexpr bool SUB = decltype(sub)::value;
+        constexpr int LOG = kLog2<SC>;
+        for (int s = 0; s < NS; ++s) {
+            const double *T = next_stage();
+            double part[R][SC];
+#pragma unroll
+            for (int dd = 0; dd < SC; ++dd) {
+                const int d = s * SC + dd;
+                double yd[R];
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    part[r][dd] = 0.0;
+                    yd[r] = SUB ? y[r][d] : 0.0;
+                }
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    const double t = T[dd * ks + jc[c]];
+#pragma unroll
+                    for (int r = 0; r < R; ++r) part[r][dd] = fma(w[r][c], SUB ? yd[r] - t : t, part[r][dd]);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const double tot = channel_sums<SC>(part[r], lane);
+                if ((lane & ((64 >> LOG) - 1)) == 0) out[r][s * SC + (lane >> (6 - LOG))] = tot;
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+    };
+    using plain = std::integral_constant<bool, false>;
+    using sub = std::integral_constant<bool, true>;
+
     // Pooled logits Qbar_i . Kbar_j / sqrt(D) (Eq. 1).
     double acc[R][CPL], P[R][CPL], S2[R][CPL];
-    column_dots<CPL, R, false>(Kt, jc, nkb, vbv, vbv, acc);
+    dot_pass(plain{}, vbv, vbv, acc);
     // Softmax over all key blocks.
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -364,18 +502,17 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
         }
     }
 
-    // Dense pooled output vbar_i = sum_j P_ij Vbar_j, w_i = S vbar_i with S the
-    // symmetric part of M (lane <-> channel), and vbar_i^T S vbar_i.
+    // Dense pooled output vbar_i = sum_j P_ij Vbar_j (over Qbar_i, no longer
+    // needed), w_i = S vbar_i with S the symmetric part of M (lane <-> channel),
+    // and vbar_i^T S vbar_i.
     double vsv[R];
     {
+        wsum_pass(plain{}, P, vbv, vbv);
         double vb[R], wv[R];
-        block_pass<CPL, R, false>(lds, P, vb, Vr, nkb, lane, vb);
-#pragma unroll
-        for (int r = 0; r < R; ++r) vbv[r][lane] = vb[r];
-        __builtin_amdgcn_wave_barrier();
         mat_vec<R, true>(Ms, vbv, wv, lane);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
+            vb[r] = vbv[r][lane];
             wvv[r][lane] = wv[r];
             vsv[r] = wave_sum(vb[r] * wv[r]);
         }
@@ -384,15 +521,17 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
 
     // q_ij = e^T M e with e = vbar_i - Vbar_j (Eq. 9), expanded through the symmetric
     // part S of M (same quadratic form): q = vbar_i^T S vbar_i - 2 Vbar_j . w_i +
-    // Vbar_j^T M Vbar_j, the last term per block from the pooling pass; one column of
-    // Vbar per candidate. s_ij = P_ij sqrt(q_ij), key_ij = s_ij / max(1 - P_ij, eps)
-    // (Eqs. 6-7).
-    column_dots<CPL, R, false>(Vt, jc, nkb, wvv, wvv, acc);
+    // Vbar_j^T M Vbar_j, the last term per block from the pooling pass.
+    // s_ij = P_ij sqrt(q_ij), key_ij = s_ij / max(1 - P_ij, eps) (Eqs. 6-7).
+    double cj[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) cj[c] = cT[jc[c]];
+    dot_pass(plain{}, wvv, wvv, acc);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-            const double q = fma(-2.0, acc[r][c], vsv[r] + cT[jc[c]]);
+            const double q = fma(-2.0, acc[r][c], vsv[r] + cj[c]);
             const double s = P[r][c] * sqrt(q > 0.0 ? q : 0.0);
             const double den = 1.0 - P[r][c];
             S2[r][c] = s * s;
@@ -429,7 +568,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
             for (int c = 0; c < CPL; ++c)
                 ko[c] = order_key(crit == RESS_CRITERION_PROBABILITY ? P[r][c]
                                   : crit == RESS_CRITERION_DRIFT_MAX_FULL ? -acc[r][c] : acc[r][c]);
-            if (CDF && crit == RESS_CRITERION_PROBABILITY && p.cdf_tau > 0.0) {
+            if (crit == RESS_CRITERION_PROBABILITY && p.cdf_tau > 0.0) {
                 // mass(n) = forced mass + the n largest candidate P: smallest n <= c_h
                 // with mass(n) >= tau by bisection (mass is non-decreasing in n).
                 double fm = 0.0;
@@ -440,7 +579,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
                 }
                 fm = wave_sum(fm);
                 auto mass = [&](int n) {
-                    const unsigned long long sel = topk_slots<CPL>(ko, memb, n, lane_bit, lane_lt);
+                    const unsigned long long sel = topk_slots<CPL>(ko, cand_bits, n, lane_lt);
                     double m = 0.0;
 #pragma unroll
                     for (int c = 0; c < CPL; ++c)
@@ -460,10 +599,8 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
                     crow[r] = max(lo, min(floor2, n_p));
                 }
             }
-            const unsigned long long keep = topk_slots<CPL>(ko, memb, crow[r], lane_bit, lane_lt);
-#pragma unroll
-            for (int c = 0; c < CPL; ++c)
-                if ((memb[c] & lane_bit) && !((keep >> c) & 1ull)) inD[r] |= 1ull << c;
+            const unsigned long long keep = topk_slots<CPL>(ko, cand_bits, crow[r], lane_lt);
+            inD[r] = cand_bits & ~keep;
         }
         double mass = 0.0;
 #pragma unroll
@@ -473,15 +610,8 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
         }
         K[r] = 1.0 - wave_sum(mass);
     }
-    {
-        double vb[R], g[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) vb[r] = vbv[r][lane];
-        block_pass<CPL, R, true>(lds, acc, vb, Vr, nkb, lane, g);
-#pragma unroll
-        for (int r = 0; r < R; ++r) gv[r][lane] = g[r];
-    }
-    double *hv[R];  // M g reuses the slot of M vbar
+    wsum_pass(sub{}, acc, vbv, gv);
+    double *hv[R];  // M g reuses the slot of S vbar
 #pragma unroll
     for (int r = 0; r < R; ++r) hv[r] = wvv[r];
     auto objective = [&]() {  // h = M g, G = g . h, J = G / max(K, eps)^2
@@ -505,7 +635,8 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
     }
 
     // Budget-neutral restoration rounds (Eqs. 13-17) with track-best. The swap
-    // count follows each row's kept count; rows whose count reached 0 are done.
+    // count follows each row's kept count; the workgroup stops once no row of it
+    // swaps anything.
     const __amdgpu_buffer_rsrc_t rsV = pooled_rsrc(Vr, nkb);
     double *swap_w = lds.swap_w();
     int *swap_j = lds.swap_j();
@@ -517,16 +648,16 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
             mrow[r] = dense[r] ? 0 : min(m, min(n_p - crow[r], crow[r]));
             mmax = max(mmax, mrow[r]);
         }
-        if (mmax <= 0) break;
+        if (!__syncthreads_or(mmax > 0)) break;
         // e_k . (M g) for every candidate k of every row.
-        column_dots<CPL, R, true>(Vt, jc, nkb, hv, vbv, acc);
+        dot_pass(sub{}, hv, vbv, acc);
         // Gains of every single restore / drop at the round-start state; the m best
         // of each kind are applied together, g and K following Eq. 13.
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int m = mrow[r];
             if (m <= 0) continue;
-            unsigned long long dj[CPL], memD[CPL], memS[CPL];
+            unsigned long long dj[CPL];
 #pragma unroll
             for (int c = 0; c < CPL; ++c) {
                 const bool in = (inD[r] >> c) & 1ull;
@@ -536,11 +667,9 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
                 const double Knh = Kn > eps ? Kn : eps;
                 const double dJ = J[r] - (G[r] + dG) / (Knh * Knh);  // Eq. 16
                 dj[c] = order_key(maximise ? -dJ : dJ);
-                memD[c] = __ballot(in);
-                memS[c] = memb[c] & ~memD[c];
             }
-            const unsigned long long rest = topk_slots<CPL>(dj, memD, m, lane_bit, lane_lt);
-            const unsigned long long drop = topk_slots<CPL>(dj, memS, m, lane_bit, lane_lt);
+            const unsigned long long rest = topk_any<CPL>(dj, inD[r], m, lane, lane_lt);
+            const unsigned long long drop = topk_any<CPL>(dj, cand_bits & ~inD[r], m, lane, lane_lt);
             inD[r] = (inD[r] & ~rest) | drop;
             double mr = 0.0, md = 0.0;
             double g = gv[r][lane];
@@ -563,8 +692,7 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
                     const int js[8] = {ja.x, ja.y, ja.z, ja.w, jb.x, jb.y, jb.z, jb.w};
                     double vj[8];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u)
-                        vj[u] = pooled_row(rsV, js[u], lane);
+                    for (int u = 0; u < 8; ++u) vj[u] = pooled_row(rsV, js[u], lane);
 #pragma unroll
                     for (int u = 0; u < 8; u += 2) {
                         const double2 w = *reinterpret_cast<const double2 *>(swap_w + t0 + u);
@@ -628,36 +756,47 @@ __global__ void __launch_bounds__(kThreads, (kMinBlocks<CPL, R>)) select_kernel(
             }
         }
     }
+    wait_vm(0);  // the ring's prefetched stages land before the workgroup ends
 }
 
-template <int CPL, int R>
+template <int CPL, int R, int NW>
 hipError_t launch_cfg(const SelectParams &p, hipStream_t s)
 {
     SelectParams q = p;
-    const int groups = (p.n_qb + kWaves * R - 1) / (kWaves * R);
+    const int groups = (p.n_qb + NW * R - 1) / (NW * R);
     q.items_per_xcd = (p.H * groups + 7) / 8;
-    if (p.cdf_tau > 0.0)  // the CDF cap has its own instantiation (it adds registers)
-        hipLaunchKernelGGL((select_kernel<CPL, R, true>), dim3((unsigned)(8 * q.items_per_xcd)), dim3(kThreads), 0, s, q);
-    else
-        hipLaunchKernelGGL((select_kernel<CPL, R, false>), dim3((unsigned)(8 * q.items_per_xcd)), dim3(kThreads), 0, s, q);
+    hipLaunchKernelGGL((select_kernel<CPL, R, NW>), dim3((unsigned)(8 * q.items_per_xcd)), dim3(NW * 64), 0, s, q);
     return hipGetLastError();
 }
 
-// Rows per wave: the most rows, up to RMAX, that still give each of the chip's
-// 256 compute units a workgroup. Measured: sharing every pooled-tensor load among
-// more rows pays only while the grid fills the chip (8 views, 86 blocks: 4 rows
-// per wave 0.20 ms, 1 row 0.12 ms; 16 views, 172 blocks: 4 rows 0.39 ms, 2 rows
-// 0.22 ms; 32 views, 344 blocks: 2 rows 0.48 ms, 1 row 0.70 ms).
+// Rows per workgroup, among 24 (12 waves of 2 rows), 16 (8 waves of 2), 8 (8
+// waves of 1) and 4 (4 waves of 1): the one with the fewest rounds of
+// workgroups over the chip's 256 compute units (one workgroup each), weighted
+// by the rows each wave carries (its serial top-k work); ties go to more
+// workgroups. Two rows per wave only up to 6 slots per lane (their candidate
+// state must fit the registers of two or three waves per SIMD); 4 waves of 1
+// row beyond 1088 key blocks.
 constexpr long long kCUs = 256;
-template <int CPL, int RMAX>
+template <int CPL, bool TWO_ROWS>
 hipError_t launch_rows(const SelectParams &p, hipStream_t s)
 {
-    auto workgroups = [&](int r) { return (long long)p.H * ((p.n_qb + kWaves * r - 1) / (kWaves * r)); };
-    if constexpr (RMAX >= 4)
-        if (workgroups(4) >= kCUs) return launch_cfg<CPL, 4>(p, s);
-    if constexpr (RMAX >= 2)
-        if (workgroups(2) >= kCUs) return launch_cfg<CPL, 2>(p, s);
-    return launch_cfg<CPL, 1>(p, s);
+    auto cost = [&](int rows, int r) {
+        const long long wg = (long long)p.H * ((p.n_qb + rows - 1) / rows);
+        return ((wg + kCUs - 1) / kCUs) * (r + 1);
+    };
+    int best = 8;
+    long long bc = cost(8, 1);
+    if (cost(4, 1) < bc) best = 4, bc = cost(4, 1);
+    if constexpr (TWO_ROWS) {
+        if (cost(16, 2) < bc) best = 16, bc = cost(16, 2);
+        if (cost(24, 2) < bc) best = 24, bc = cost(24, 2);
+    }
+    if constexpr (TWO_ROWS) {
+        if (best == 24) return launch_cfg<CPL, 2, 12>(p, s);
+        if (best == 16) return launch_cfg<CPL, 2, 8>(p, s);
+    }
+    if (best == 8) return launch_cfg<CPL, 1, 8>(p, s);
+    return launch_cfg<CPL, 1, 4>(p, s);
 }
 
 }  // namespace
@@ -666,17 +805,14 @@ hipError_t launch_select(const SelectParams &p, hipStream_t s)
 {
     if (p.H == 0 || p.n_qb == 0) return hipSuccess;
     const int n = p.n_kb;
-    if (n <= 64) return launch_rows<1, 4>(p, s);
-    if (n <= 128) return launch_rows<2, 4>(p, s);
-    if (n <= 256) return launch_rows<4, 4>(p, s);
-    if (n <= 384) return launch_rows<6, 2>(p, s);
-    if (n <= 512) return launch_cfg<8, 1>(p, s);
-    if (n <= 768) return launch_cfg<12, 1>(p, s);
-    if (n <= 1088) return launch_cfg<17, 1>(p, s);
-    if (n <= 1536) return launch_cfg<24, 1>(p, s);
-    if (n <= 2048) return launch_cfg<32, 1>(p, s);
-    if (n <= 3072) return launch_cfg<48, 1>(p, s);
-    return launch_cfg<64, 1>(p, s);
+    if (n <= 128) return launch_rows<2, true>(p, s);
+    if (n <= 256) return launch_rows<4, true>(p, s);
+    if (n <= 384) return launch_rows<6, true>(p, s);
+    if (n <= 512) return launch_rows<8, false>(p, s);
+    if (n <= 768) return launch_rows<12, false>(p, s);
+    if (n <= 1088) return launch_rows<17, false>(p, s);
+    if (n <= 2048) return launch_cfg<32, 1, 4>(p, s);
+    return launch_cfg<64, 1, 4>(p, s);
 }
 
 }  // namespace ress

@@ -318,40 +318,51 @@ def test_config_layer_stack(ress, layer):
     _config_case(ress, stack_layer(layer), 5, n_tokens=128, label=f"16v layer {layer}")
 
 
-def _rows_per_wave(H, n_qb, n_kb):
-    """Rows per wave the selection launch takes: at most 4 (<= 256 key blocks), 2
-    (<= 384) or 1, and within that the most that still give each of the 256
-    compute units a workgroup of 4 waves."""
-    cap = 4 if n_kb <= 256 else 2 if n_kb <= 384 else 1
-    for r in (4, 2):
-        if r <= cap and H * -(-n_qb // (4 * r)) >= 256:
-            return r
-    return 1
+def _launch_shape(H, n_qb, n_kb):
+    """Selection launch the library takes: slots per lane by key-block count, then
+    rows per workgroup 16 (8 waves of 2 rows, up to 384 key blocks), 8 (8 waves
+    of 1, up to 1088) or 4 (4 waves of 1), the most that still give each of the
+    256 compute units a workgroup."""
+    for lim, cpl, two in ((128, 2, True), (256, 4, True), (384, 6, True), (512, 8, False), (768, 12, False),
+                          (1088, 17, False), (2048, 32, None), (4096, 64, None)):
+        if n_kb <= lim:
+            break
+    if two is None:
+        return cpl, 4
+    wg = lambda rows: H * -(-n_qb // rows)
+    if two and wg(16) >= 256:
+        return cpl, 16
+    return (cpl, 8) if wg(8) >= 256 else (cpl, 4)
 
 
-# (views, patch tokens per view, heads, slots per lane, rows per wave), 64-token blocks:
-# every launch shape of the selection up to 384 key blocks.
-LAUNCH_SHAPES = [(4, 1019, 64, 1, 4), (4, 1019, 32, 1, 2), (4, 1019, 16, 1, 1),
-                 (8, 1019, 32, 2, 4), (8, 1019, 16, 2, 2), (8, 1019, 8, 2, 1),
-                 (8, 2043, 16, 4, 4), (8, 2043, 8, 4, 2), (8, 2043, 4, 4, 1),
-                 (8, 3067, 8, 6, 2), (8, 3067, 4, 6, 1)]
+# (key blocks of 64 tokens, heads, slots per lane, rows per workgroup): every launch
+# shape of the selection.
+LAUNCH_SHAPES = [(120, 32, 2, 16), (120, 24, 2, 8), (120, 8, 2, 4),
+                 (200, 20, 4, 16), (200, 16, 4, 8), (200, 8, 4, 4),
+                 (350, 12, 6, 16), (350, 8, 6, 8), (350, 4, 6, 4),
+                 (450, 6, 8, 8), (450, 4, 8, 4),
+                 (700, 4, 12, 8), (700, 2, 12, 4),
+                 (1000, 4, 17, 8), (1000, 2, 17, 4),
+                 (1500, 2, 32, 4),
+                 (3000, 1, 64, 4)]
 
 
-@pytest.mark.parametrize("views,ppv,H,cpl,rpw", LAUNCH_SHAPES)
-def test_select_launch_shapes(ress, views, ppv, H, cpl, rpw):
-    """Each (slots per lane, rows per wave) shape against the oracle on a row
-    sample, also with the probability rule under a CDF cap (its own build)."""
-    L = synth.make_layer(views, ppv, 5, H=H, block=64, sparsity=0.75, seed=40 + cpl * 4 + rpw,
-                         name=f"{views}v H={H}")
-    assert -(-L.n_kb // 64) == cpl and _rows_per_wave(L.H, L.n_qb, L.n_kb) == rpw
-    say(f"[select launch shape] slots {cpl}, rows per wave {rpw}: H={L.H} N={L.N} n_kb={L.n_kb}")
-    rng = np.random.default_rng(cpl * 10 + rpw)
-    rows = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 120), [0, L.n_qb - 1, L.H * L.n_qb - 1]]))
+@pytest.mark.parametrize("n_kb,H,cpl,rows", LAUNCH_SHAPES)
+def test_select_launch_shapes(ress, n_kb, H, cpl, rows):
+    """Each (slots per lane, rows per workgroup) launch against the oracle on a row
+    sample, with the drift rule and with the probability rule under a binding CDF
+    cap."""
+    L = synth.make_layer(8, n_kb * 8 - 5, 5, H=H, block=64, sparsity=0.75, seed=40 + cpl * 4 + rows,
+                         name=f"{n_kb} blocks H={H}")
+    assert L.n_kb == n_kb and _launch_shape(L.H, L.n_qb, L.n_kb) == (cpl, rows)
+    say(f"[select launch shape] slots {cpl}, rows per workgroup {rows}: H={L.H} N={L.N} n_kb={L.n_kb}")
+    rng = np.random.default_rng(cpl * 10 + rows)
+    rows_s = np.unique(np.concatenate([rng.integers(0, L.H * L.n_qb, 120), [0, L.n_qb - 1, L.H * L.n_qb - 1]]))
     gpu, _ = gpu_select(L, rounds=5)
-    compare_select(L, gpu, oracle_select(L, rounds=5, rows=rows), rows=rows, label=f"{cpl}x{rpw}")
+    compare_select(L, gpu, oracle_select(L, rounds=5, rows=rows_s), rows=rows_s, label=f"{cpl}x{rows}")
     gpu, _ = gpu_select(L, rounds=3, criterion=1, cdf_tau=0.25)  # the cap binds on most rows here
-    compare_select(L, gpu, oracle_select(L, rounds=3, rows=rows, criterion=1, cdf_tau=0.25), rows=rows,
-                   label=f"{cpl}x{rpw} cdf", criterion=1, capped=True)
+    compare_select(L, gpu, oracle_select(L, rounds=3, rows=rows_s, criterion=1, cdf_tau=0.25), rows=rows_s,
+                   label=f"{cpl}x{rows} cdf", criterion=1, capped=True)
 
 
 def test_dense_attention_32v_sampled(ress):
