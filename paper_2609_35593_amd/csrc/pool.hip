@@ -124,7 +124,7 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
     // Channel-major outputs: thread (row, w) writes block j0 + w of channel row.
     const int row = t >> 2, w = t & 3;
     if (w < nb) {
-        const size_t off = ((size_t)h * kD + row) * p.out.kstride + j0 + w;
+        const size_t off = pooled_pair_index(h, row, j0 + w, p.out.kstride);
         (is_v ? p.out.vbarT : p.out.kbarT)[off] = tile[row][w];
     }
 }

@@ -11,12 +11,12 @@
 //  - Every pass over the head's pooled tensors (the pooled logits against
 //    Kbar, then the dense pooled output, the drift scores, the net drift and
 //    every round's gains against Vbar) streams the channel-major tensor through
-//    LDS once per workgroup: stages of SC channel rows move global -> LDS by DMA
+//    LDS once per workgroup: stages of SC channels (whole channel pairs) move global -> LDS by DMA
 //    (global_load_lds, 1 KB per wave instruction, no registers held) into a ring
 //    of 3 to 6 slots, each stage issued as far ahead of its use as the ring
 //    allows, with one workgroup barrier per stage;
-//    each wave then reads its key blocks of every channel row from LDS (64
-//    consecutive doubles per read: no bank conflicts). All rows of the
+//    each wave then reads its key blocks of every channel pair from LDS (16
+//    bytes per lane, 64 consecutive: no bank conflicts). All rows of the
 //    workgroup share every stage, so the tensors cross L2 once per NW x R rows.
 //  - The weighted sums over key blocks (vbar = sum_j P_j Vbar_j, g = sum over the
 //    drop set) are formed per lane over its slots and combined across the wave
@@ -40,16 +40,14 @@ typedef __attribute__((address_space(3))) void lds_void;
 // no swizzle, no index stride): loads past num_records bytes return zero.
 constexpr int kBufWord3 = 0x00020000;
 
-// Channel rows per stage: the most (a power of two up to 8) whose stage of
-// 64 CPL key blocks fits 36 KB; one row (up to 32 KB) for the largest rows.
-// Larger stages keep more bytes in flight per barrier (the passes over long
-// rows are bound by the DMA round trip, not by arithmetic).
+// Channels per stage (whole channel pairs): the most (up to 8) whose stage of 64
+// CPL key blocks fits 36 KB, at least one pair (64 KB for 4096-block rows).
 template <int CPL>
-constexpr int kSC = (CPL * 512 * 8 <= 36864) ? 8 : (CPL * 512 * 4 <= 36864) ? 4 : (CPL * 512 * 2 <= 36864) ? 2 : 1;
+constexpr int kSC = (CPL * 512 * 8 <= 36864) ? 8 : (CPL * 512 * 4 <= 36864) ? 4 : 2;
 template <int SC>
 constexpr int kLog2 = SC == 8 ? 3 : SC == 4 ? 2 : SC == 2 ? 1 : 0;
 // Bytes of one ring slot, and the number of slots: as many as the LDS left by
-// the wave areas and M_h holds, from 3 up to 6 (each stage is issued slots - 1
+// the wave areas and M_h holds, from 2 up to 6 (each stage is issued slots - 1
 // stages ahead of its use).
 template <int CPL>
 constexpr int kSlotBytes = (CPL * 512 * kSC<CPL> + 1023) / 1024 * 1024;
@@ -300,7 +298,7 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     constexpr int SB = kSlotBytes<CPL>;                    // bytes per ring slot
     constexpr int OTHER = NW * WaveLds<R>::kDoubles * 8 + kD * (kD + 1) * 4 + 2048;
     constexpr int NB = kNBuf<CPL, OTHER>;                  // ring slots
-    static_assert(NB >= 3, "at least three ring slots");
+    static_assert(NB >= 2, "at least two ring slots");
     __shared__ __attribute__((aligned(1024))) unsigned char ring[NB * SB];
     __shared__ __align__(16) double wareas[NW * WaveLds<R>::kDoubles];
     __shared__ float Ms[kD * (kD + 1)];
@@ -316,10 +314,11 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     const int row0 = (item % groups) * NW * R + wave * R;
     const int nkb = p.n_kb, nqb = p.n_qb, ks = p.pooled.kstride;
 
-    // Stage k of the workgroup's sequence holds channel rows (k mod NS) SC ..
-    // +SC-1 of Kbar^T for the first pass and of Vbar^T for every later one. Each
-    // wave issues its share of the stage's 1 KB DMA instructions; lanes past the
-    // stage's end re-read its last 16 bytes (in bounds) into the slot's slack.
+    // Stage k of the workgroup's sequence holds channels (k mod NS) SC .. +SC-1
+    // (SC / 2 channel pairs, contiguous) of Kbar^T for the first pass and of
+    // Vbar^T for every later one. Each wave issues its share of the stage's 1 KB
+    // DMA instructions; lanes past the stage's end re-read its last 16 bytes (in
+    // bounds) into the slot's slack.
     const unsigned char *Kt = reinterpret_cast<const unsigned char *>(p.pooled.kbarT + (size_t)h * kD * ks);
     const unsigned char *Vt = reinterpret_cast<const unsigned char *>(p.pooled.vbarT + (size_t)h * kD * ks);
     const int sbytes = SC * ks * (int)sizeof(double);
@@ -394,42 +393,27 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
 #pragma unroll
             for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
         for (int s = 0; s < NS; ++s) {
-            const double *T = next_stage();
-            if constexpr (SC == 1) {
-                double xd[R], yd[R];
+            const double2 *T = reinterpret_cast<const double2 *>(next_stage());
+            // Channel pairs one at a time (registers for two waves per SIMD or more);
+            // one 16-byte read gives both channels of a pair for a key block.
+#pragma unroll 1
+            for (int pp = 0; pp < SC / 2; ++pp) {
+                const int d = s * SC + 2 * pp;
+                double2 xd[R], yd[R];
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
-                    xd[r] = x[r][s];
-                    yd[r] = SUB ? y[r][s] : 0.0;
+                    xd[r] = *reinterpret_cast<const double2 *>(x[r] + d);
+                    if (SUB) yd[r] = *reinterpret_cast<const double2 *>(y[r] + d);
                 }
 #pragma unroll
                 for (int c = 0; c < CPL; ++c) {
-                    const double t = T[jc[c]];
-#pragma unroll
-                    for (int r = 0; r < R; ++r)
-                        acc[r][c] = SUB ? fma(yd[r] - t, xd[r], acc[r][c]) : fma(xd[r], t, acc[r][c]);
-                }
-            } else {
-                // Channel pairs one at a time (registers for two waves per SIMD or more).
-#pragma unroll 1
-                for (int dd = 0; dd < SC; dd += 2) {
-                    const int d = s * SC + dd;
-                    double2 xd[R], yd[R];
+                    const double2 t = T[pp * ks + jc[c]];
 #pragma unroll
                     for (int r = 0; r < R; ++r) {
-                        xd[r] = *reinterpret_cast<const double2 *>(x[r] + d);
-                        if (SUB) yd[r] = *reinterpret_cast<const double2 *>(y[r] + d);
-                    }
-#pragma unroll
-                    for (int c = 0; c < CPL; ++c) {
-                        const double t0 = T[dd * ks + jc[c]], t1 = T[(dd + 1) * ks + jc[c]];
-#pragma unroll
-                        for (int r = 0; r < R; ++r) {
-                            if (SUB)
-                                acc[r][c] = fma(yd[r].y - t1, xd[r].y, fma(yd[r].x - t0, xd[r].x, acc[r][c]));
-                            else
-                                acc[r][c] = fma(xd[r].y, t1, fma(xd[r].x, t0, acc[r][c]));
-                        }
+                        if (SUB)
+                            acc[r][c] = fma(yd[r].y - t.y, xd[r].y, fma(yd[r].x - t.x, xd[r].x, acc[r][c]));
+                        else
+                            acc[r][c] = fma(xd[r].y, t.y, fma(xd[r].x, t.x, acc[r][c]));
                     }
                 }
             }
@@ -443,22 +427,26 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
         constexpr bool SUB = decltype(sub)::value;
         constexpr int LOG = kLog2<SC>;
         for (int s = 0; s < NS; ++s) {
-            const double *T = next_stage();
+            const double2 *T = reinterpret_cast<const double2 *>(next_stage());
             double part[R][SC];
 #pragma unroll
-            for (int dd = 0; dd < SC; ++dd) {
-                const int d = s * SC + dd;
-                double yd[R];
+            for (int pp = 0; pp < SC / 2; ++pp) {
+                const int d = s * SC + 2 * pp;
+                double2 yd[R];
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
-                    part[r][dd] = 0.0;
-                    yd[r] = SUB ? y[r][d] : 0.0;
+                    part[r][2 * pp] = 0.0;
+                    part[r][2 * pp + 1] = 0.0;
+                    yd[r] = SUB ? *reinterpret_cast<const double2 *>(y[r] + d) : double2{0.0, 0.0};
                 }
 #pragma unroll
                 for (int c = 0; c < CPL; ++c) {
-                    const double t = T[dd * ks + jc[c]];
+                    const double2 t = T[pp * ks + jc[c]];
 #pragma unroll
-                    for (int r = 0; r < R; ++r) part[r][dd] = fma(w[r][c], SUB ? yd[r] - t : t, part[r][dd]);
+                    for (int r = 0; r < R; ++r) {
+                        part[r][2 * pp] = fma(w[r][c], SUB ? yd[r].x - t.x : t.x, part[r][2 * pp]);
+                        part[r][2 * pp + 1] = fma(w[r][c], SUB ? yd[r].y - t.y : t.y, part[r][2 * pp + 1]);
+                    }
                 }
             }
 #pragma unroll
