@@ -167,8 +167,9 @@ def criteria_report(ress, L, q, k, v, gram, o_dense, stream):
     criterion the median pooled drift J of the returned selection (over rows that
     drop blocks) and the token-level residual drift it leaves,
     sum ||W_O (O_sparse - O_dense)||^2 / sum ||W_O O_dense||^2 over every token and
-    head, with ||W_O x||^2 = x^T M x. Everything runs in this library's kernels;
-    the residual drift is reduced with torch."""
+    head, with ||W_O x||^2 = x^T M x. Everything runs in this library's kernels
+    (the norms per query block in ress_block_drift_sq); torch only adds up the
+    per-block sums."""
     import torch
 
     cases = [("drift, R=5 (ReSS)", 0, 0.0, 5), ("drift, R=0", 0, 0.0, 0), ("probability top-k", 1, 0.0, 0),
@@ -176,14 +177,14 @@ def criteria_report(ress, L, q, k, v, gram, o_dense, stream):
              ("drift maximised, full", 3, 0.0, 5)]
     gram32 = gram.float()
     od = o_dense.float()
-    base = torch.einsum("htd,hde,hte->", od, gram32, od).item()
+    zero = torch.zeros_like(od)
+    base = ress.ress_block_drift_sq(od, zero, gram32, bq=L.bq, stream=stream).sum().item()
     rep = []
     for label, crit, tau, rounds in cases:
         sel = ress.ress_select(q, k, v, gram, L.budgets, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
                                rounds=rounds, criterion=crit, cdf_tau=tau, stream=stream)
         o = ress.ress_sparse_attn(q, k, v, sel["kept_count"], sel["kept_idx"], bq=L.bq, bk=L.bk, stream=stream)
-        d = o.float() - od
-        resid = torch.einsum("htd,hde,hte->", d, gram32, d).item()
+        resid = ress.ress_block_drift_sq(o.float(), od, gram32, bq=L.bq, stream=stream).sum().item()
         dr = sel["drift"].reshape(-1, 2)
         live = dr[:, 0] > 0
         kept = sel["kept_count"].sum().item()

@@ -186,6 +186,21 @@ int ress_sparse_attn_out_f32(const ress_shape *shape, const void *q, const void 
                              const int32_t *kept_count, const int32_t *kept_idx, float scale, float *o,
                              hipStream_t stream);
 
+/* The change masking makes in what attention writes into the residual
+ * stream, per query block: the reference measurement of Sec. 3 ("Testing the
+ * Probability Assumption", Fig. 2), which masks one key block and compares the
+ * attention outputs after the output projection. For every head h and query
+ * block i,
+ *   out[h][i] = sum over the block's tokens t of (a_t - b_t)^T M_h (a_t - b_t)
+ *             = sum_t ||W_O^h (a_t - b_t)||^2,
+ * in float64, with a and b two attention outputs of the same queries (for
+ * instance ress_sparse_attn_out_f32 with every key block but j, and with all).
+ *   a, b   device float32 [H][N][64], 16-byte aligned
+ *   gram   device float32 [H][64][64] (M_h), 16-byte aligned
+ *   out    device float64 [H][n_qb] out (must not alias the inputs) */
+int ress_block_drift_sq(const ress_shape *shape, const float *a, const float *b, const float *gram, double *out,
+                        hipStream_t stream);
+
 /* Dense attention, the same computation over every key block of every row
  * (the baseline the paper compares against, Table S6). */
 int ress_dense_attn(const ress_shape *shape, const void *q, const void *k, const void *v,

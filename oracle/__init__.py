@@ -331,3 +331,20 @@ def head_major_rows(o, tokens=None):
     H, n, D = x.shape
     return x.transpose(1, 0, 2).reshape(n, H * D)
 
+
+def block_drift_sq(a, b, gram, *, bq: int):
+    """Per query block i of head h, the sum over its tokens t of
+    (a_t - b_t)^T M_h (a_t - b_t) = ||W_O^h (a_t - b_t)||^2 (the masking
+    measurement of Sec. 3), in float64; a, b float [H][N][D], gram [H][D][D].
+    Returns float64 [H][n_qb]."""
+    x = np.asarray(a, dtype=np.float64) - np.asarray(b, dtype=np.float64)
+    M = np.asarray(gram, dtype=np.float64)
+    H, N, _ = x.shape
+    n_qb = (N + bq - 1) // bq
+    out = np.zeros((H, n_qb))
+    for h in range(H):
+        q = np.einsum("td,de,te->t", x[h], M[h], x[h])
+        for i in range(n_qb):
+            out[h, i] = q[i * bq:min((i + 1) * bq, N)].sum()
+    return out
+

@@ -64,6 +64,8 @@ def _load():
     L.ress_select_noalloc.argtypes = [C.POINTER(ress_shape), C.POINTER(ress_select_params), vp, vp, vp, vp, vp, vp,
                                       vp, vp, vp, vp, vp]
     L.ress_select_noalloc.restype = i
+    L.ress_block_drift_sq.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp]
+    L.ress_block_drift_sq.restype = i
     L.ress_sparse_attn.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, f, vp, vp]
     L.ress_sparse_attn.restype = i
     L.ress_sparse_attn_out_f32.argtypes = [C.POINTER(ress_shape), vp, vp, vp, vp, vp, f, vp, vp]
@@ -343,6 +345,25 @@ def ress_out_proj_residual_f32(o, w_o, resid_in, *, resid_out=None, stream=None)
     if st != RESS_OK:
         raise RessError(st, "ress_out_proj_residual_f32")
     return resid_out
+
+
+def ress_block_drift_sq(a, b, gram, *, bq: int, out=None, stream=None):
+    """Per query block sum over its tokens of (a_t - b_t)^T M_h (a_t - b_t) (see
+    include/ress.h). a, b: float32 [H][N][64]; gram: float32 [H][64][64].
+    Returns float64 [H][n_qb]."""
+    H, N, D = a.shape
+    dev = a.device
+    for name, t in (("a", a), ("b", b)):
+        _check_out(name, t, torch.float32, (H, N, D), dev)
+    _check_out("gram", gram, torch.float32, (H, D, D), dev)
+    n_qb = (N + bq - 1) // bq
+    out = torch.empty((H, n_qb), dtype=torch.float64, device=dev) if out is None else out
+    _check_out("out", out, torch.float64, (H, n_qb), dev)
+    shape = make_shape(H, N, bq=bq, bk=bq, D=D)
+    st = lib.ress_block_drift_sq(C.byref(shape), _ptr(a), _ptr(b), _ptr(gram), _ptr(out), _stream(stream, dev))
+    if st != RESS_OK:
+        raise RessError(st, "ress_block_drift_sq")
+    return out
 
 
 def bf16_from_bits(bits: np.ndarray, device) -> torch.Tensor:

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libress.so")
 OBJ_DIR = os.path.join(HERE, "_build")
-SOURCES = ["pool.hip", "select.hip", "attn.hip", "proj.hip", "ress_api.cpp"]
+SOURCES = ["pool.hip", "select.hip", "attn.hip", "proj.hip", "drift.hip", "ress_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-ffp-contract=fast",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

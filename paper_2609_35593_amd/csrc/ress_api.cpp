@@ -319,6 +319,30 @@ int ress_out_proj_residual_f32(const ress_shape *shape, const void *o, const voi
     return RESS_OK;
 }
 
+int ress_block_drift_sq(const ress_shape *shape, const float *a, const float *b, const float *gram, double *out,
+                        hipStream_t stream)
+{
+    Grid g;
+    int st = check_shape(shape, &g);
+    if (st != RESS_OK) return st;
+    if (!has_work(shape)) return RESS_OK;
+    if (!a || !b || !gram || !out) return RESS_E_INVALID_ARG;
+    if (!aligned16(a) || !aligned16(b) || !aligned16(gram)) return RESS_E_INVALID_ARG;
+    if ((const void *)out == a || (const void *)out == b || (const void *)out == gram) return RESS_E_INVALID_ARG;
+    if ((long long)shape->H * g.n_qb > 0x7fffffffLL) return RESS_E_UNSUPPORTED;
+    ress::DriftSqParams dp;
+    dp.H = shape->H;
+    dp.N = shape->N;
+    dp.bq = shape->bq;
+    dp.n_qb = (int)g.n_qb;
+    dp.a = a;
+    dp.b = b;
+    dp.gram = gram;
+    dp.out = out;
+    if (ress::launch_drift_sq(dp, stream) != hipSuccess) return RESS_E_HIP;
+    return RESS_OK;
+}
+
 static int attn_common(const ress_shape *shape, const void *q, const void *k, const void *v,
                        const int32_t *kept_count, const int32_t *kept_idx, float scale, void *o,
                        bool sparse, bool out_f32, hipStream_t stream)

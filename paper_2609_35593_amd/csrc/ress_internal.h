@@ -85,7 +85,17 @@ struct ProjParams {
     Pooled pooled;            // mode 0
 };
 
+// Per-query-block squared projected norm of the difference of two float32
+// attention outputs (the masking reference of Sec. 3).
+struct DriftSqParams {
+    int H, N, bq, n_qb;
+    const float *a, *b;   // [H][N][64]
+    const float *gram;    // [H][64][64]
+    double *out;          // [H][n_qb]
+};
+
 hipError_t launch_pool(const PoolParams &p, hipStream_t s);
+hipError_t launch_drift_sq(const DriftSqParams &p, hipStream_t s);
 hipError_t launch_proj(const ProjParams &p, hipStream_t s);
 hipError_t launch_select(const SelectParams &p, hipStream_t s);
 hipError_t launch_attn(const AttnParams &p, int bq, int bk, bool sparse, hipStream_t s);

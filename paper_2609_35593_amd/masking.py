@@ -4,7 +4,8 @@ For each key block j, every query block attends to all key blocks except j
 (ress_sparse_attn_out_f32 with the list B minus j), and the change in what
 attention writes into the residual stream is measured against the unmasked
 output: for query block i of head h, the Euclidean norm over its tokens t of
-W_O^h (O_t(B minus j) - O_t(B)), using ||W_O^h x||^2 = x^T M_h x. Ranking the
+W_O^h (O_t(B minus j) - O_t(B)), using ||W_O^h x||^2 = x^T M_h x
+(ress_block_drift_sq). Ranking the
 candidate blocks of a row by this change and by a selection criterion (pooled
 probability, or the drift score of Eqs. 5-7) and taking the Spearman
 correlation gives the comparison of Fig. 2.
@@ -14,7 +15,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import ress_sparse_attn_out_f32
+from . import ress_block_drift_sq, ress_sparse_attn_out_f32
 
 
 def block_masking_change(q, k, v, gram, *, bq: int, bk: int, blocks=None, stream=None) -> np.ndarray:
@@ -31,17 +32,15 @@ def block_masking_change(q, k, v, gram, *, bq: int, bk: int, blocks=None, stream
     base = ress_sparse_attn_out_f32(q, k, v, count_all, kept_all, bq=bq, bk=bk, stream=stream)
     masked = torch.empty_like(base)
     M = gram.to(device=dev, dtype=torch.float32).contiguous()
-    pad = n_qb * bq - N
-    out = torch.empty((H, n_qb, len(blocks)), dtype=torch.float64, device=dev)
+    sq = torch.empty((H, n_qb), dtype=torch.float64, device=dev)
+    out = np.empty((H, n_qb, len(blocks)))
     for col, j in enumerate(blocks):
         lst = torch.cat([every[:j], every[j + 1:], torch.full((1,), -1, dtype=torch.int32, device=dev)])
         kept = lst.expand(H, n_qb, n_kb).contiguous()
         ress_sparse_attn_out_f32(q, k, v, count_drop, kept, bq=bq, bk=bk, out=masked, stream=stream)
-        d = masked - base
-        per_token = (torch.bmm(d, M) * d).sum(-1)  # d^T M d, [H][N]
-        per_token = torch.nn.functional.pad(per_token, (0, pad))
-        out[:, :, col] = per_token.view(H, n_qb, bq).sum(-1).double().clamp_min(0).sqrt()
-    return out.cpu().numpy()
+        ress_block_drift_sq(masked, base, M, bq=bq, out=sq, stream=stream)
+        out[:, :, col] = np.sqrt(np.maximum(sq.cpu().numpy(), 0.0))
+    return out
 
 
 def _ranks(x: np.ndarray) -> np.ndarray:

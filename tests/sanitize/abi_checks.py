@@ -31,6 +31,7 @@ lib.ress_dense_attn.argtypes = [C.POINTER(Shape), vp, vp, vp, C.c_float, vp, vp]
 lib.ress_qkv_proj_pool.argtypes = [C.POINTER(Shape)] + [vp] * 7 + [sz, vp]
 lib.ress_out_proj_residual.argtypes = [C.POINTER(Shape)] + [vp] * 5
 lib.ress_out_proj_residual_f32.argtypes = [C.POINTER(Shape)] + [vp] * 5
+lib.ress_block_drift_sq.argtypes = [C.POINTER(Shape)] + [vp] * 5
 lib.ress_status_string.restype = C.c_char_p
 
 checks = 0
@@ -86,4 +87,6 @@ expect(lib.ress_qkv_proj_pool(C.byref(sh4), p[0], p[1], p[0], p[3], p[4], p[5], 
        "q aliases x")
 expect(lib.ress_out_proj_residual(C.byref(sh4), p[0], p[1], p[2], p[0], None), INVALID, "resid_out aliases o")
 expect(lib.ress_out_proj_residual_f32(C.byref(sh4), p[0], p[1], None, p[3], None), INVALID, "no resid_in")
+expect(lib.ress_block_drift_sq(C.byref(sh4), None, p[1], p[2], p[3], None), INVALID, "drift sq null")
+expect(lib.ress_block_drift_sq(C.byref(sh4), p[0], p[1], p[2], p[0], None), INVALID, "drift sq aliasing")
 print(f"abi checks ok: {checks}", flush=True)

@@ -8,4 +8,5 @@ hipError_t launch_pool(const PoolParams &, hipStream_t) { return hipErrorInvalid
 hipError_t launch_proj(const ProjParams &, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_select(const SelectParams &, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_attn(const AttnParams &, int, int, bool, hipStream_t) { return hipErrorInvalidValue; }
+hipError_t launch_drift_sq(const DriftSqParams &, hipStream_t) { return hipErrorInvalidValue; }
 }  // namespace ress

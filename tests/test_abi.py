@@ -26,7 +26,8 @@ def ress():
 
 
 def test_header_declares_the_boundary():
-    assert declared_entry_points() == ["ress_dense_attn", "ress_out_proj_residual", "ress_out_proj_residual_f32",
+    assert declared_entry_points() == ["ress_block_drift_sq", "ress_dense_attn", "ress_out_proj_residual",
+                                       "ress_out_proj_residual_f32",
                                        "ress_qkv_proj_pool", "ress_select", "ress_select_noalloc",
                                        "ress_select_workspace_size", "ress_sparse_attn", "ress_sparse_attn_out_f32",
                                        "ress_status_string"]
@@ -191,3 +192,17 @@ def test_select_with_pooled_state_needs_no_qkv(ress):
     st = ress.lib.ress_select(C.byref(shape), C.byref(params), None, None, None, p, budget.ctypes.data, p, p, None,
                               None, None, C.c_void_p(1 << 40), need, None)
     assert st == ress.RESS_E_INVALID_ARG
+
+
+def test_block_drift_sq_checks(ress):
+    """ress_block_drift_sq rejects null, misaligned and aliasing arguments on the
+    host (nothing reaches the GPU) and does nothing without work."""
+    f = ress.lib.ress_block_drift_sq
+    sh = ress.make_shape(4, 1000, bq=128, bk=128)
+    p = [C.c_void_p((1 << 41) + (n << 30)) for n in range(4)]
+    assert f(C.byref(sh), None, p[1], p[2], p[3], None) == ress.RESS_E_INVALID_ARG
+    assert f(C.byref(sh), p[0], p[1], p[2], None, None) == ress.RESS_E_INVALID_ARG
+    assert f(C.byref(sh), C.c_void_p((1 << 41) + 4), p[1], p[2], p[3], None) == ress.RESS_E_INVALID_ARG
+    assert f(C.byref(sh), p[0], p[1], p[2], p[0], None) == ress.RESS_E_INVALID_ARG  # out aliases a
+    assert f(C.byref(ress.make_shape(4, 1000, bq=96, bk=128)), p[0], p[1], p[2], p[3], None) == ress.RESS_E_UNSUPPORTED
+    assert f(C.byref(ress.make_shape(4, 0, bq=128, bk=128)), None, None, None, None, None) == ress.RESS_OK

@@ -131,3 +131,23 @@ def test_residual_stream_16v_stack(ress):
     say(f"  end to end vs the oracle's attention: relative norm error {rel_b:.3e}; "
         f"||r_L|| / ||sum_l W_O O_dense|| = {drift:.4f}; median J per layer {np.round(jmed, 5).tolist()}")
     assert np.all(np.isfinite(got)) and 0.0 < drift < 1.0
+
+
+@pytest.mark.parametrize("H,N,bq", [(3, 1000, 128), (2, 150, 64), (16, 2755, 128)])
+def test_block_drift_sq(ress, H, N, bq):
+    """ress_block_drift_sq against the float64 oracle: the differences of float32
+    values are exact in float64, so only the order of the float64 sums differs."""
+    import torch
+
+    say(f"[block drift sq] H={H} N={N} bq={bq}")
+    rng = np.random.default_rng(H * 100 + bq)
+    a = (rng.standard_normal((H, N, 64)) * 0.3).astype(np.float32)
+    b = a + (rng.standard_normal((H, N, 64)) * 1e-3).astype(np.float32)
+    _, gram = synth.draw_w_o(H, 64, 5)
+    dev = "cuda:0"
+    got = ress.ress_block_drift_sq(torch.from_numpy(a).to(dev), torch.from_numpy(b).to(dev),
+                                   torch.from_numpy(gram).to(dev), bq=bq)
+    torch.cuda.synchronize()
+    ref = oracle.block_drift_sq(a, b, gram, bq=bq)
+    np.testing.assert_allclose(got.cpu().numpy(), ref, rtol=1e-12, atol=0)
+

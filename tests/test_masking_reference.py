@@ -70,3 +70,24 @@ def test_product_rank_correlation_matches_the_oracle():
     for r in range(4):
         ref = oracle.spearman(a[r], b[r])
         assert (math.isnan(ref) and math.isnan(got[r])) or got[r] == pytest.approx(ref, abs=1e-12)
+
+
+def test_block_drift_sq_is_the_projected_norm():
+    """The per-block masking change: with M = I it is the plain squared norm, with
+    the generator's M_h = W_O^h^T W_O^h it is ||W_O^h x||^2 with the materialised
+    W_O^h (up to M_h's float32 rounding), summed over each block's tokens
+    (partial last block included)."""
+    rng = np.random.default_rng(3)
+    H, N, bq = 2, 150, 64
+    a = rng.standard_normal((H, N, 64)).astype(np.float32)
+    b = rng.standard_normal((H, N, 64)).astype(np.float32)
+    x = a.astype(np.float64) - b.astype(np.float64)
+    eye = np.broadcast_to(np.eye(64, dtype=np.float32), (H, 64, 64))
+    got = oracle.block_drift_sq(a, b, eye, bq=bq)
+    want = np.array([[np.sum(x[h, i * bq:min((i + 1) * bq, N)] ** 2) for i in range(3)] for h in range(H)])
+    np.testing.assert_allclose(got, want, rtol=1e-13)
+    w, gram = synth.draw_w_o(H, 64, 11)
+    got = oracle.block_drift_sq(a, b, gram, bq=bq)
+    want = np.array([[np.sum((x[h, i * bq:min((i + 1) * bq, N)] @ w[h].T) ** 2) for i in range(3)] for h in range(H)])
+    np.testing.assert_allclose(got, want, rtol=1e-6)
+
