@@ -2,9 +2,9 @@
 // plus c_j = Vbar_j^T M_h Vbar_j for the drift scores (Eq. 9).
 //
 // One wave per pooled block; a workgroup holds 4 waves that pool 4 consecutive
-// blocks of the same head and tensor, so the channel-major outputs are written
-// 4 blocks (32 bytes) at a time and, for V, the head's M_h is staged in LDS once
-// for 4 blocks. Lane l streams the 16-byte chunk l/8 (channels 8(l/8)..+7) of
+// blocks of the same head and tensor, so that for V the head's M_h is staged in
+// LDS once for 4 blocks. Outputs are row-major (lane t writes channel t). Lane l
+// streams the 16-byte chunk l/8 (channels 8(l/8)..+7) of
 // tokens l%8, l%8 + 8, ...: every load instruction of a wave covers 8 whole
 // 128-byte token rows, and a block is one batch of independent loads. Partial
 // sums are float64; the 8 lanes of a chunk are combined with a fixed butterfly,
@@ -69,7 +69,6 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
 {
     __shared__ float Ms[kD * (kD + 1)];       // M_h, padded rows (V workgroups)
     __shared__ double vb[kWaves][kD];         // each wave's Vbar_j
-    __shared__ double tile[kD][kWaves];       // channel-major outputs of the 4 blocks
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
     const int gq = (p.n_qb + kWaves - 1) / kWaves, gk = (p.n_kb + kWaves - 1) / kWaves;
@@ -86,7 +85,6 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
     const bool is_v = g >= gq + gk;
     const int j0 = (is_v ? g - gq - gk : g - gq) * kWaves;
     const int j = j0 + wave;
-    const int nb = min(kWaves, p.n_kb - j0);  // blocks of this workgroup
     constexpr int MPT = kD * kD / 4 / kThreads;  // float4 pieces of M_h per thread
     float4 mreg[MPT];
     if (is_v) {  // issued before the block loads, stored to LDS after them
@@ -97,11 +95,8 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
     if (j < p.n_kb) {
         const int lo = j * p.bk, cnt = min(p.bk, p.N - lo);
         const double mean = wave_block_mean(is_v ? p.v : p.k, (size_t)h * p.N + lo, cnt);
-        if (is_v) {
-            p.out.vbar[((size_t)h * p.n_kb + j) * kD + lane] = mean;
-            vb[wave][lane] = mean;
-        }
-        tile[lane][wave] = mean;
+        (is_v ? p.out.vbar : p.out.kbar)[((size_t)h * p.n_kb + j) * kD + lane] = mean;
+        if (is_v) vb[wave][lane] = mean;
     }
     if (is_v) {  // M_h row r, column c at r * 65 + c
 #pragma unroll
@@ -120,12 +115,6 @@ __global__ void __launch_bounds__(kThreads) pool_kernel(const PoolParams p)
         for (int c = 0; c < kD; ++c) u = fma((double)Ms[lane * (kD + 1) + c], vb[wave][c], u);
         const double cj = wave_sum(u * vb[wave][lane]);
         if (lane == 0) p.out.cT[(size_t)h * p.n_kb + j] = cj;
-    }
-    // Channel-major outputs: thread (row, w) writes block j0 + w of channel row.
-    const int row = t >> 2, w = t & 3;
-    if (w < nb) {
-        const size_t off = pooled_pair_index(h, row, j0 + w, p.out.kstride);
-        (is_v ? p.out.vbarT : p.out.kbarT)[off] = tile[row][w];
     }
 }
 

@@ -230,10 +230,9 @@ __global__ void __launch_bounds__(kThreads, 1) proj_kernel(const ProjParams p)
             if (which == 0) {
                 p.pooled.qbar[((size_t)h * p.n_qb + blk_g) * 64 + d] = mean;
             } else if (which == 1) {
-                p.pooled.kbarT[pooled_pair_index(h, d, blk_g, p.pooled.kstride)] = mean;
+                p.pooled.kbar[((size_t)h * p.n_kb + blk_g) * 64 + d] = mean;
             } else {
                 p.pooled.vbar[((size_t)h * p.n_kb + blk_g) * 64 + d] = mean;
-                p.pooled.vbarT[pooled_pair_index(h, d, blk_g, p.pooled.kstride)] = mean;
                 vmean[blk * BN + c] = mean;
             }
         }

@@ -39,24 +39,22 @@ bool has_work(const ress_shape *s) { return s->H > 0 && s->N > 0; }
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 bool aligned16(const void *ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 
-// Workspace: qbar [H][n_qb][64], kbarT [H][64][ks], vbar [H][n_kb][64], vbarT
-// [H][64][ks], cT [H][n_kb] (float64, ks = n_kb rounded up to even), every
-// region 256-byte aligned.
+// Workspace: qbar [H][n_qb][64], kbar [H][n_kb][64], vbar [H][n_kb][64], cT
+// [H][n_kb] (float64), every region 256-byte aligned.
 struct Regions {
-    size_t qb, kt, vb, cb;
+    size_t qb, kb, cb;  // qbar; kbar and vbar (each); cT
 };
 
 Regions regions(const ress_shape *s, const Grid &g)
 {
-    const size_t ks = (size_t)ress::pooled_kstride((int)g.n_kb);
-    return {align256((size_t)s->H * g.n_qb * kD * sizeof(double)), align256((size_t)s->H * kD * ks * sizeof(double)),
-            align256((size_t)s->H * g.n_kb * kD * sizeof(double)), align256((size_t)s->H * g.n_kb * sizeof(double))};
+    return {align256((size_t)s->H * g.n_qb * kD * sizeof(double)), align256((size_t)s->H * g.n_kb * kD * sizeof(double)),
+            align256((size_t)s->H * g.n_kb * sizeof(double))};
 }
 
 size_t workspace_bytes(const ress_shape *s, const Grid &g)
 {
     const Regions r = regions(s, g);
-    return r.qb + 2 * r.kt + r.vb + r.cb;
+    return r.qb + 2 * r.kb + r.cb;
 }
 
 // Pooled state inside the workspace (the regions workspace_bytes sizes).
@@ -66,11 +64,9 @@ ress::Pooled pooled_layout(const ress_shape *s, const Grid &g, void *workspace)
     const Regions r = regions(s, g);
     ress::Pooled pooled;
     pooled.qbar = reinterpret_cast<double *>(w);
-    pooled.kbarT = reinterpret_cast<double *>(w + r.qb);
-    pooled.vbar = reinterpret_cast<double *>(w + r.qb + r.kt);
-    pooled.vbarT = reinterpret_cast<double *>(w + r.qb + r.kt + r.vb);
-    pooled.cT = reinterpret_cast<double *>(w + r.qb + 2 * r.kt + r.vb);
-    pooled.kstride = ress::pooled_kstride((int)g.n_kb);
+    pooled.kbar = reinterpret_cast<double *>(w + r.qb);
+    pooled.vbar = reinterpret_cast<double *>(w + r.qb + r.kb);
+    pooled.cT = reinterpret_cast<double *>(w + r.qb + 2 * r.kb);
     return pooled;
 }
 

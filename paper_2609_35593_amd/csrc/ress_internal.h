@@ -12,26 +12,14 @@ namespace ress {
 constexpr int kD = 64;      // head dimension handled by every kernel
 constexpr int kWave = 64;   // CDNA wavefront width
 
-// Pooled tensors of one layer, float64, carved out of the selection workspace.
-// The channel-major tensors hold channel pairs: element (d, j) of head h at
-// ((h * 32 + d / 2) * kstride + j) * 2 + d % 2, so that the two channels of a
-// pair for one key block are one 16-byte read; kstride = n_kb rounded up to even.
+// Pooled tensors of one layer, float64, row-major, carved out of the selection
+// workspace.
 struct Pooled {
-    double *qbar;   // [H][n_qb][64]          query block means
-    double *kbarT;  // [H][32][kstride][2]    key block means, channel-pair-major
-    double *vbar;   // [H][n_kb][64]          value block means
-    double *vbarT;  // [H][32][kstride][2]    value block means, channel-pair-major
-    double *cT;     // [H][n_kb]              Vbar_j^T M_h Vbar_j
-    int kstride;
+    double *qbar;   // [H][n_qb][64]  query block means
+    double *kbar;   // [H][n_kb][64]  key block means
+    double *vbar;   // [H][n_kb][64]  value block means
+    double *cT;     // [H][n_kb]      Vbar_j^T M_h Vbar_j
 };
-
-// Index of element (d, j) of head h in a channel-pair-major pooled tensor.
-__host__ __device__ inline size_t pooled_pair_index(int h, int d, int j, int kstride)
-{
-    return (((size_t)h * 32 + (d >> 1)) * kstride + j) * 2 + (d & 1);
-}
-
-__host__ __device__ inline int pooled_kstride(int n_kb) { return (n_kb + 1) & ~1; }
 
 struct PoolParams {
     int H, N, bq, bk, n_qb, n_kb;

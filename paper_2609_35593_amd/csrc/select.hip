@@ -7,26 +7,21 @@
 //  - Per-candidate quantities live "lane <-> key block": lane l, slot c holds key
 //    block j = l + 64 c (CPL slots). Per-row vectors (Qbar, vbar, S vbar with S
 //    the symmetric part of M, g, M g) live in the wave's LDS area, channel d at
-//    index d, and are read as broadcasts.
-//  - Every pass over the head's pooled tensors (the pooled logits against
-//    Kbar, then the dense pooled output, the drift scores, the net drift and
-//    every round's gains against Vbar) streams the channel-major tensor through
-//    LDS once per workgroup: stages of SC channels (whole channel pairs) move global -> LDS by DMA
-//    (global_load_lds, 1 KB per wave instruction, no registers held) into a ring
-//    of 3 to 6 slots, each stage issued as far ahead of its use as the ring
-//    allows, with one workgroup barrier per stage;
-//    each wave then reads its key blocks of every channel pair from LDS (16
-//    bytes per lane, 64 consecutive: no bank conflicts). All rows of the
-//    workgroup share every stage, so the tensors cross L2 once per NW x R rows.
-//  - The weighted sums over key blocks (vbar = sum_j P_j Vbar_j, g = sum over the
-//    drop set) are formed per lane over its slots and combined across the wave
-//    by a butterfly that halves the channels each lane carries at every step.
+//    index d.
+//  - The contractions are float64 matrix products of the workgroup's rows
+//    (padded to a multiple of 16) with the head's row-major pooled tensors, on
+//    the matrix cores (16x16x4 float64 steps): over channels, the pooled logits
+//    against Kbar and the drift scores and every round's gains against Vbar;
+//    over key blocks, the dense pooled output vbar and the net drift g against
+//    Vbar. The pooled tensor goes from L2 straight into the B operands (each lane
+//    reads 16 contiguous bytes or more of one key block); the A operands are the
+//    rows' LDS vectors, or their weights staged in LDS; result tiles pass through
+//    the LDS staging area into the layout of the owning wave. Each output element
+//    is one chain of matrix steps in a fixed order: reruns are bit-identical.
 //  - Every top-k is exact: a bitwise search for the k-th largest of
 //    order-preserving 64-bit keys, using wave ballots and popcounts, ties broken
-//    by the lower block index. No atomics and no data-dependent reduction
-//    order: reruns are bit-identical.
-// All arithmetic is float64: CDNA4 runs float64 FMA at the rate of unpacked
-// float32, and it keeps the discrete decisions stable.
+//    by the lower block index. No atomics and no data-dependent reduction order.
+// All arithmetic is float64 (the discrete decisions stay stable).
 #include <math.h>
 
 #include "ress_internal.h"
@@ -34,57 +29,32 @@
 namespace ress {
 namespace {
 
-typedef __attribute__((address_space(3))) void lds_void;
+typedef double v4d __attribute__((ext_vector_type(4)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
 // Word 3 of a raw buffer descriptor on gfx9-family chips (32-bit data format,
 // no swizzle, no index stride): loads past num_records bytes return zero.
 constexpr int kBufWord3 = 0x00020000;
 
-// Channels per stage (whole channel pairs): the most (up to 8) whose stage of 64
-// CPL key blocks fits 36 KB, at least one pair (64 KB for 4096-block rows).
-template <int CPL>
-constexpr int kSC = (CPL * 512 * 8 <= 36864) ? 8 : (CPL * 512 * 4 <= 36864) ? 4 : 2;
-template <int SC>
-constexpr int kLog2 = SC == 8 ? 3 : SC == 4 ? 2 : SC == 2 ? 1 : 0;
-// Bytes of one ring slot, and the number of slots: as many as the LDS left by
-// the wave areas and M_h holds, from 2 up to 6 (each stage is issued slots - 1
-// stages ahead of its use).
-template <int CPL>
-constexpr int kSlotBytes = (CPL * 512 * kSC<CPL> + 1023) / 1024 * 1024;
-template <int CPL, int OTHER>
-constexpr int kNBuf = ((163840 - OTHER) / kSlotBytes<CPL>) > 6 ? 6 : ((163840 - OTHER) / kSlotBytes<CPL>);
-
-// Wait until at most n (0..63) of this wave's vector memory operations are
-// outstanding (loads complete in issue order: everything older than the last n
-// has landed). The count is an immediate of s_waitcnt, hence the dispatch.
-template <int N>
-__device__ __forceinline__ void wait_vm_dispatch(int n)
-{
-    if constexpr (N < 64) {
-        if (n == N) {
-            __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
-            return;
-        }
-        wait_vm_dispatch<N + 1>(n);
-    } else {
-        __builtin_amdgcn_s_waitcnt(0x0F70);  // out of range: wait for everything
-    }
-}
-__device__ __forceinline__ void wait_vm(int n) { wait_vm_dispatch<0>(n); }
-
-// Buffer descriptor over one head's row-major pooled Vbar (n_kb x 64 doubles).
+// Buffer descriptor over one head's row-major pooled tensor (nkb x 64 doubles).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t pooled_rsrc(const double *base, int nkb)
 {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<double *>(base), 0, kD * nkb * (int)sizeof(double),
                                              kBufWord3);
 }
 
-// Channel `lane` of row j (wave-uniform) of the row-major pooled Vbar.
+// Channel `lane` of row j (wave-uniform) of a row-major pooled tensor.
 __device__ __forceinline__ double pooled_row(__amdgpu_buffer_rsrc_t rs, int j, int lane)
 {
     return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(
                                           rs, (unsigned)lane * (unsigned)sizeof(double),
                                           __builtin_amdgcn_readfirstlane(j) * kD * (int)sizeof(double), 0));
+}
+
+// 16 bytes at byte offset `off` of a pooled tensor (zero past its end).
+__device__ __forceinline__ double2 pooled_16(__amdgpu_buffer_rsrc_t rs, int off)
+{
+    return __builtin_bit_cast(double2, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
 }
 
 __device__ __forceinline__ double wave_sum(double x)
@@ -101,38 +71,9 @@ __device__ __forceinline__ double wave_max(double x)
     return x;
 }
 
-// Sum over the wave of N per-lane values v[0..N-1] (channel dd of a stage):
-// log2(N) exchange steps each keep half of the channels (the lane with the mask
-// bit set keeps the upper half and receives its partner's upper half), then a
-// plain butterfly over the remaining lanes. Lane l returns the total of channel
-// l >> (6 - log2 N); fixed order, identical across the lanes sharing it. Every
-// index is a compile-time constant (the values stay in registers).
-template <int N, int M>
-__device__ __forceinline__ double channel_sums_step(const double (&v)[N], int lane)
+__device__ __forceinline__ v4d mfma_f64(double a, double b, v4d c)
 {
-    if constexpr (N == 1) {
-        double x = v[0];
-#pragma unroll
-        for (int m = M; m >= 1; m >>= 1) x += __shfl_xor(x, m);
-        return x;
-    } else {
-        constexpr int H = N / 2;
-        const bool hi = (lane & M) != 0;
-        double w[H];
-#pragma unroll
-        for (int i = 0; i < H; ++i) {
-            const double send = hi ? v[i] : v[H + i];
-            const double keep = hi ? v[H + i] : v[i];
-            w[i] = keep + __shfl_xor(send, M);
-        }
-        return channel_sums_step<H, M / 2>(w, lane);
-    }
-}
-
-template <int SC>
-__device__ __forceinline__ double channel_sums(const double (&v)[SC], int lane)
-{
-    return channel_sums_step<SC, 32>(v, lane);
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
 }
 
 // Order-preserving map of a double to uint64 (larger value -> larger key);
@@ -290,70 +231,164 @@ __device__ __forceinline__ void mat_vec(const float *Ms, double *const (&y)[R], 
     }
 }
 
+// Sizes of a workgroup configuration: RW rows in MT 16-row tiles; the LDS
+// staging area holds 16 MT rows of CHK slots (64 key blocks each) plus 2 doubles
+// of padding per row (so that rows start on different 16-byte bank groups), as
+// many slots as the LDS left by the wave areas and M_h allows.
+template <int CPL, int R, int NW>
+struct SelCfg {
+    static constexpr int RW = NW * R;
+    static constexpr int MT = (RW + 15) / 16;
+    static constexpr int WD = WaveLds<R>::kDoubles;
+    static constexpr int FIXED = NW * WD * 8 + kD * (kD + 1) * 4 + 256;
+    static constexpr int chk()
+    {
+        int c = CPL;
+        while (c > 1 && FIXED + 16 * MT * (c * 512 + 16) > 163840) --c;
+        return c;
+    }
+    static constexpr int CHK = chk();
+    static constexpr int SROW = CHK * 64 + 2;          // doubles per staging row
+    static constexpr int NCH = (CPL + CHK - 1) / CHK;  // chunks of slots
+    static_assert(2 * MT <= NW, "one weighted-sum item per wave at most");
+};
+
 template <int CPL, int R, int NW>
 __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p)
 {
-    constexpr int SC = kSC<CPL>;                           // channel rows per stage
-    constexpr int NS = kD / SC;                            // stages per pass
-    constexpr int SB = kSlotBytes<CPL>;                    // bytes per ring slot
-    constexpr int OTHER = NW * WaveLds<R>::kDoubles * 8 + kD * (kD + 1) * 4 + 2048;
-    constexpr int NB = kNBuf<CPL, OTHER>;                  // ring slots
-    static_assert(NB >= 2, "at least two ring slots");
-    __shared__ __attribute__((aligned(1024))) unsigned char ring[NB * SB];
-    __shared__ __align__(16) double wareas[NW * WaveLds<R>::kDoubles];
+    using Cfg = SelCfg<CPL, R, NW>;
+    constexpr int RW = Cfg::RW, MT = Cfg::MT, CHK = Cfg::CHK, SROW = Cfg::SROW, NCH = Cfg::NCH;
+    __shared__ __align__(16) double stage[16 * MT * SROW];
+    __shared__ __align__(16) double wareas[NW * Cfg::WD];
     __shared__ float Ms[kD * (kD + 1)];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const unsigned long long lane_lt = (1ull << lane) - 1ull;
     // Workgroups are numbered so that each of the 8 XCDs gets a contiguous range
     // of (head, row group) items: the rows of a head share one XCD's L2.
-    const int groups = (p.n_qb + NW * R - 1) / (NW * R);
+    const int groups = (p.n_qb + RW - 1) / RW;
     const int item = (blockIdx.x & 7) * p.items_per_xcd + (blockIdx.x >> 3);
     if (item >= p.H * groups) return;  // the whole workgroup
     const int h = item / groups;
-    const int row0 = (item % groups) * NW * R + wave * R;
-    const int nkb = p.n_kb, nqb = p.n_qb, ks = p.pooled.kstride;
-
-    // Stage k of the workgroup's sequence holds channels (k mod NS) SC .. +SC-1
-    // (SC / 2 channel pairs, contiguous) of Kbar^T for the first pass and of
-    // Vbar^T for every later one. Each wave issues its share of the stage's 1 KB
-    // DMA instructions; lanes past the stage's end re-read its last 16 bytes (in
-    // bounds) into the slot's slack.
-    const unsigned char *Kt = reinterpret_cast<const unsigned char *>(p.pooled.kbarT + (size_t)h * kD * ks);
-    const unsigned char *Vt = reinterpret_cast<const unsigned char *>(p.pooled.vbarT + (size_t)h * kD * ks);
-    const int sbytes = SC * ks * (int)sizeof(double);
-    const int ninstr = (sbytes + 1023) >> 10;
-    const int mine = (ninstr - wave + NW - 1) / NW;  // this wave's DMA instructions per stage
-    auto issue = [&](int k) __attribute__((always_inline)) {
-        const unsigned char *src = (k < NS ? Kt : Vt) + (size_t)(k % NS) * sbytes;
-        unsigned char *dst = ring + (k % NB) * SB;
-        for (int u = wave; u < ninstr; u += NW) {
-            const int off = min(u * 1024 + lane * 16, sbytes - 16);
-            __builtin_amdgcn_global_load_lds((const void *)(src + off), (lds_void *)(dst + u * 1024), 16, 0, 0);
-        }
-    };
-    int kc = 0;  // next stage to consume
-    for (int k = 0; k < NB - 1; ++k) issue(k);
+    const int row0 = (item % groups) * RW + wave * R;
+    const int nkb = p.n_kb, nqb = p.n_qb;
+    const int ntiles = (nkb + 15) >> 4;
+    const __amdgpu_buffer_rsrc_t rsK = pooled_rsrc(p.pooled.kbar + (size_t)h * nkb * kD, nkb);
+    const __amdgpu_buffer_rsrc_t rsV = pooled_rsrc(p.pooled.vbar + (size_t)h * nkb * kD, nkb);
     {
         const float *Mh = p.gram + (size_t)h * kD * kD;
         for (int e = tid; e < kD * kD; e += NW * 64) Ms[(e >> 6) * (kD + 1) + (e & 63)] = Mh[e];
     }
-    // Stage kc is ready for every wave once this wave's DMAs older than the
-    // NB - 2 stages issued after it have landed and the workgroup has met (which
-    // also frees the slot of stage kc + NB - 1, last read as stage kc - 1); then
-    // stage kc + NB - 1 is issued.
-    auto next_stage = [&]() __attribute__((always_inline)) -> const double * {
-        wait_vm((NB - 2) * mine);
+    // Vector `slot` of the workgroup's row m (in the area of the wave owning it).
+    auto row_vec = [&](int slot, int m) -> double * {
+        return wareas + (m / R) * Cfg::WD + (slot * R + m % R) * kD;
+    };
+    const int grp = lane >> 4, col = lane & 15;  // matrix-step lane coordinates
+
+    // acc[r][c] = sum_d X_m[d] T_j[d] for this wave's rows m and key blocks
+    // j = lane + 64 c, with X_m vector `xs` of row m and T the head's pooled tensor
+    // behind rs. Tiles of 16 key blocks go round the waves; for tile t, lane l holds
+    // channels 16 (l / 16) .. +15 of key block 16 t + l % 16 (in step s the k index
+    // l / 16 stands for channel 16 (l / 16) + s, in A as in B) and the tile is
+    // multiplied with every 16-row tile of the workgroup (rows past RW repeat the
+    // last one; their results are not read). Results reach the owners through the
+    // staging area, CHK slots at a time.
+    auto dot_pass = [&](int xs, __amdgpu_buffer_rsrc_t rs, double (&acc)[R][CPL]) __attribute__((always_inline)) {
+        const double *arow[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) arow[mt] = row_vec(xs, min(16 * mt + col, RW - 1)) + 16 * grp;
+#pragma unroll
+        for (int q = 0; q < NCH; ++q) {
+            const int t0 = 4 * CHK * q, t1 = min(4 * CHK * (q + 1), ntiles);
+            for (int t = t0 + (wave - t0 % NW + NW) % NW; t < t1; t += NW) {  // tile t: wave t mod NW
+                double b[16];
+                const int off = (16 * t + col) * kD * (int)sizeof(double) + grp * 128;
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const double2 v = pooled_16(rs, off + 16 * u);
+                    b[2 * u] = v.x;
+                    b[2 * u + 1] = v.y;
+                }
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    v4d c = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const double2 a = *reinterpret_cast<const double2 *>(arow[mt] + 2 * u);
+                        c = mfma_f64(a.x, b[2 * u], c);
+                        c = mfma_f64(a.y, b[2 * u + 1], c);
+                    }
+                    // c[v] = C[16 mt + 4 v + l / 16][16 t + l % 16]
+                    double *dst = stage + (16 * mt + grp) * SROW + (16 * t - 64 * CHK * q) + col;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) dst[4 * v * SROW] = c[v];
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int c = 0; c < CPL; ++c)
+                if (c / CHK == q)
+#pragma unroll
+                    for (int r = 0; r < R; ++r) acc[r][c] = stage[(wave * R + r) * SROW + (c - CHK * q) * 64 + lane];
+            __syncthreads();
+        }
+    };
+    // out_m[d] = sum_j w_m(j) Vbar_j[d] for every row m of the workgroup, into vector
+    // `os` of row m, with w_m(j) = w[r][c] of the owning wave (zero for key blocks
+    // past n_kb). The owners stage their weights CHK slots at a time; item
+    // (mt, np) = (wave / 2, wave % 2) accumulates the 16 rows of tile mt against
+    // channels 32 np + 2 n + e (n < 16, e = 0, 1) over all key blocks: in each
+    // step the k index l / 16 stands for key block 8 o + 2 (l / 16) + (0 or 1) of
+    // the octet o, so that one 16-byte read gives the A values of two steps and
+    // one 16-byte read of a key block's channel pair the B values of two products.
+    auto wsum_pass = [&](const double (&w)[R][CPL], int os) __attribute__((always_inline)) {
+        const bool mine = wave < 2 * MT;
+        const int mt = wave >> 1, np = wave & 1;
+        v4d c0 = {0.0, 0.0, 0.0, 0.0}, c1 = c0;
+        const double *arow = stage + (16 * mt + col) * SROW + 2 * grp;
+        const int boff = (32 * np + 2 * col) * (int)sizeof(double);
+#pragma unroll
+        for (int q = 0; q < NCH; ++q) {
+#pragma unroll
+            for (int c = 0; c < CPL; ++c)
+                if (c / CHK == q)
+#pragma unroll
+                    for (int r = 0; r < R; ++r) stage[(wave * R + r) * SROW + (c - CHK * q) * 64 + lane] = w[r][c];
+            __syncthreads();
+            const int kq = min(64 * CHK, nkb - 64 * CHK * q);  // key blocks of the chunk
+            if (mine && kq > 0) {
+                const int noct = (kq + 7) >> 3;
+                const int key0 = 64 * CHK * q + 2 * grp;
+#pragma unroll 2
+                for (int o = 0; o < noct; ++o) {
+                    const double2 a = *reinterpret_cast<const double2 *>(arow + 8 * o);
+                    const int key = key0 + 8 * o;
+                    const double2 b0 = pooled_16(rsV, key * kD * (int)sizeof(double) + boff);
+                    const double2 b1 = pooled_16(rsV, (key + 1) * kD * (int)sizeof(double) + boff);
+                    c0 = mfma_f64(a.x, b0.x, c0);
+                    c1 = mfma_f64(a.x, b0.y, c1);
+                    c0 = mfma_f64(a.y, b1.x, c0);
+                    c1 = mfma_f64(a.y, b1.y, c1);
+                }
+            }
+            __syncthreads();
+        }
+        // c_e[v] = out[row 16 mt + 4 v + l / 16][channel 32 np + 2 (l % 16) + e]
+        if (mine) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int m = 16 * mt + 4 * v + grp;
+                if (m < RW) {
+                    double *o = row_vec(os, m) + 32 * np + 2 * col;
+                    *reinterpret_cast<double2 *>(o) = double2{c0[v], c1[v]};
+                }
+            }
+        }
         __syncthreads();
-        issue(kc + NB - 1);
-        const double *T = reinterpret_cast<const double *>(ring + (kc % NB) * SB);
-        ++kc;
-        return T;
     };
 
-    const WaveLds<R> lds{wareas + wave * WaveLds<R>::kDoubles};
+    const WaveLds<R> lds{wareas + wave * Cfg::WD};
     const double eps = p.eps;
-    const double *Vr = p.pooled.vbar + (size_t)h * nkb * kD;
     const double *cT = p.pooled.cT + (size_t)h * nkb;
     const int c_h = p.budgets[h];
     const int n_p = p.first_forced;  // candidates are the key blocks j < first_forced
@@ -381,88 +416,11 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
         jc[c] = valid[c] ? j : nkb - 1;
         if (j < n_p) cand_bits |= 1ull << c;
     }
-    __builtin_amdgcn_wave_barrier();
-
-    // acc[r][c] = sum_d x_r[d] T[d][j_c], or with SUB sum_d (y_r[d] - T[d][j_c]) x_r[d],
-    // in ascending d, over one pass of the ring.
-    auto dot_pass = [&](auto sub, double *const (&x)[R], double *const (&y)[R],
-                        double (&acc)[R][CPL]) __attribute__((always_inline)) {
-        constexpr bool SUB = decltype(sub)::value;
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) acc[r][c] = 0.0;
-        for (int s = 0; s < NS; ++s) {
-            const double2 *T = reinterpret_cast<const double2 *>(next_stage());
-            // Channel pairs one at a time (registers for two waves per SIMD or more);
-            // one 16-byte read gives both channels of a pair for a key block.
-#pragma unroll 1
-            for (int pp = 0; pp < SC / 2; ++pp) {
-                const int d = s * SC + 2 * pp;
-                double2 xd[R], yd[R];
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    xd[r] = *reinterpret_cast<const double2 *>(x[r] + d);
-                    if (SUB) yd[r] = *reinterpret_cast<const double2 *>(y[r] + d);
-                }
-#pragma unroll
-                for (int c = 0; c < CPL; ++c) {
-                    const double2 t = T[pp * ks + jc[c]];
-#pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        if (SUB)
-                            acc[r][c] = fma(yd[r].y - t.y, xd[r].y, fma(yd[r].x - t.x, xd[r].x, acc[r][c]));
-                        else
-                            acc[r][c] = fma(xd[r].y, t.y, fma(xd[r].x, t.x, acc[r][c]));
-                    }
-                }
-            }
-        }
-    };
-    // out_r[d] = sum_j w_r(j) T[d][j], or with SUB sum_j w_r(j) (y_r[d] - T[d][j]),
-    // for every channel d, into the wave's LDS vector out_r: per lane over its
-    // slots in ascending order, then across the wave (channel_sums).
-    auto wsum_pass = [&](auto sub, const double (&w)[R][CPL], double *const (&y)[R],
-                         double *const (&out)[R]) __attribute__((always_inline)) {
-        constexpr bool SUB = decltype(sub)::value;
-        constexpr int LOG = kLog2<SC>;
-        for (int s = 0; s < NS; ++s) {
-            const double2 *T = reinterpret_cast<const double2 *>(next_stage());
-            double part[R][SC];
-#pragma unroll
-            for (int pp = 0; pp < SC / 2; ++pp) {
-                const int d = s * SC + 2 * pp;
-                double2 yd[R];
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    part[r][2 * pp] = 0.0;
-                    part[r][2 * pp + 1] = 0.0;
-                    yd[r] = SUB ? *reinterpret_cast<const double2 *>(y[r] + d) : double2{0.0, 0.0};
-                }
-#pragma unroll
-                for (int c = 0; c < CPL; ++c) {
-                    const double2 t = T[pp * ks + jc[c]];
-#pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        part[r][2 * pp] = fma(w[r][c], SUB ? yd[r].x - t.x : t.x, part[r][2 * pp]);
-                        part[r][2 * pp + 1] = fma(w[r][c], SUB ? yd[r].y - t.y : t.y, part[r][2 * pp + 1]);
-                    }
-                }
-            }
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const double tot = channel_sums<SC>(part[r], lane);
-                if ((lane & ((64 >> LOG) - 1)) == 0) out[r][s * SC + (lane >> (6 - LOG))] = tot;
-            }
-        }
-        __builtin_amdgcn_wave_barrier();
-    };
-    using plain = std::integral_constant<bool, false>;
-    using sub = std::integral_constant<bool, true>;
+    __syncthreads();  // M_h and every row's Qbar in place
 
     // Pooled logits Qbar_i . Kbar_j / sqrt(D) (Eq. 1).
     double acc[R][CPL], P[R][CPL], S2[R][CPL];
-    dot_pass(plain{}, vbv, vbv, acc);
+    dot_pass(0, rsK, acc);
     // Softmax over all key blocks.
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -495,7 +453,7 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     // and vbar_i^T S vbar_i.
     double vsv[R];
     {
-        wsum_pass(plain{}, P, vbv, vbv);
+        wsum_pass(P, 0);
         double vb[R], wv[R];
         mat_vec<R, true>(Ms, vbv, wv, lane);
 #pragma unroll
@@ -504,7 +462,7 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
             wvv[r][lane] = wv[r];
             vsv[r] = wave_sum(vb[r] * wv[r]);
         }
-        __builtin_amdgcn_wave_barrier();
+        __syncthreads();  // every row's w in place
     }
 
     // q_ij = e^T M e with e = vbar_i - Vbar_j (Eq. 9), expanded through the symmetric
@@ -514,7 +472,7 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     double cj[CPL];
 #pragma unroll
     for (int c = 0; c < CPL; ++c) cj[c] = cT[jc[c]];
-    dot_pass(plain{}, wvv, wvv, acc);
+    dot_pass(1, rsV, acc);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
 #pragma unroll
@@ -544,7 +502,7 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     const int crit = p.criterion;
     const bool maximise = crit == RESS_CRITERION_DRIFT_MAX_SWAP || crit == RESS_CRITERION_DRIFT_MAX_FULL;
     unsigned long long inD[R], best[R];
-    double K[R], G[R], J[R], J0[R], Jb[R];
+    double K[R], G[R], J[R], J0[R], Jb[R], msum[R];
     int crow[R];  // kept candidates of the row
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -596,9 +554,13 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
             acc[r][c] = ((inD[r] >> c) & 1ull) ? P[r][c] : 0.0;  // weights of the g pass
             mass += acc[r][c];
         }
-        K[r] = 1.0 - wave_sum(mass);
+        msum[r] = wave_sum(mass);
+        K[r] = 1.0 - msum[r];
     }
-    wsum_pass(sub{}, acc, vbv, gv);
+    // g = sum_{j in D} P_j (vbar - Vbar_j) = (sum_{j in D} P_j) vbar - sum_{j in D} P_j Vbar_j
+    wsum_pass(acc, 2);
+#pragma unroll
+    for (int r = 0; r < R; ++r) gv[r][lane] = fma(msum[r], vbv[r][lane], -gv[r][lane]);
     double *hv[R];  // M g reuses the slot of S vbar
 #pragma unroll
     for (int r = 0; r < R; ++r) hv[r] = wvv[r];
@@ -625,7 +587,6 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     // Budget-neutral restoration rounds (Eqs. 13-17) with track-best. The swap
     // count follows each row's kept count; the workgroup stops once no row of it
     // swaps anything.
-    const __amdgpu_buffer_rsrc_t rsV = pooled_rsrc(Vr, nkb);
     double *swap_w = lds.swap_w();
     int *swap_j = lds.swap_j();
     for (int rr = 0; rr < p.rounds; ++rr) {
@@ -637,8 +598,14 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
             mmax = max(mmax, mrow[r]);
         }
         if (!__syncthreads_or(mmax > 0)) break;
-        // e_k . (M g) for every candidate k of every row.
-        dot_pass(sub{}, hv, vbv, acc);
+        // e_k . (M g) = vbar . (M g) - Vbar_k . (M g) for every candidate k of every row.
+        dot_pass(1, rsV, acc);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const double vmg = wave_sum(vbv[r][lane] * hv[r][lane]);
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) acc[r][c] = vmg - acc[r][c];
+        }
         // Gains of every single restore / drop at the round-start state; the m best
         // of each kind are applied together, g and K following Eq. 13.
 #pragma unroll
@@ -744,7 +711,6 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
             }
         }
     }
-    wait_vm(0);  // the ring's prefetched stages land before the workgroup ends
 }
 
 template <int CPL, int R, int NW>

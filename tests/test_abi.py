@@ -58,8 +58,8 @@ def test_workspace_size(ress):
     st, n = _ws(ress)
     assert st == 0
     align = lambda x: (x + 255) // 256 * 256
-    # qbar, kbarT, vbar, vbarT (float64 [16][344][64]) and the per-block quadratic term [16][344]
-    assert n == align(16 * 344 * 64 * 8) + 3 * align(16 * 344 * 64 * 8) + align(16 * 344 * 8)
+    # qbar, kbar, vbar (float64 [16][344][64]) and the per-block quadratic term [16][344]
+    assert n == 3 * align(16 * 344 * 64 * 8) + align(16 * 344 * 8)
     assert _ws(ress, N=0, n_special_tail=0) == (0, 0)
     assert _ws(ress, H=0) == (0, 0)
     assert _ws(ress, N=4096 * 128, H=1, n_special_tail=0)[0] == 0
