@@ -87,44 +87,89 @@ __device__ __forceinline__ unsigned long long order_key(double x)
 // Exact top-k of the member slots by (key desc, block index asc). Bit c of
 // mbits marks this lane's slot c as a member. Non-member keys are replaced by 0,
 // below every member key (an order key of a finite value is at least 1), so one
-// ballot per slot counts members only. Returns this lane's chosen slots as a
-// bit mask. Requires 0 <= k <= number of members.
+// ballot per slot counts members only. The k-th largest key is found bit by
+// bit, high word first: while the low word of a candidate threshold is zero, a
+// key reaches it exactly when its high word does. Once the high word t of the
+// k-th largest key is known, a key reaches a candidate (t, x) (x >= 1) exactly
+// when the 32-bit value "all ones if its high word is above t, its low word if
+// equal, zero if below" reaches x. Every count is wave-uniform (scalar
+// registers); the search stops as soon as exactly k keys reach the threshold.
+// Returns this lane's chosen slots as a bit mask. Requires 0 <= k <= number of
+// members.
 template <int CPL>
 __device__ __forceinline__ unsigned long long topk_slots(const unsigned long long (&key)[CPL],
                                                          unsigned long long mbits, int k, unsigned long long lane_lt)
 {
+    k = __builtin_amdgcn_readfirstlane(k);
     if (k <= 0) return 0ull;
-    unsigned long long km[CPL];
+    unsigned int hi[CPL], lo[CPL];
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) km[c] = ((mbits >> c) & 1ull) ? key[c] : 0ull;
-    unsigned long long thr = 0;  // invariant: #members with key >= thr is >= k
-    bool exact = false;
-    for (int b = 63; b >= 0; --b) {
-        const unsigned long long cand = thr | (1ull << b);
+    for (int c = 0; c < CPL; ++c) {
+        const unsigned long long km = ((mbits >> c) & 1ull) ? key[c] : 0ull;
+        hi[c] = (unsigned int)(km >> 32);
+        lo[c] = (unsigned int)km;
+    }
+    // High word: invariant #members with high word >= thi is >= k. The
+    // threshold, the bit and the counts are wave-uniform and the loop has a
+    // single exit, so that it runs on scalar registers and scalar branches.
+    unsigned int thi = 0, bit = 0x80000000u;
+    int found = 0;
+    do {
+        const unsigned int cand = __builtin_amdgcn_readfirstlane(thi | bit);
+        unsigned long long bl[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) bl[c] = __ballot(hi[c] >= cand);
         int cnt = 0;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) cnt += __popcll(__ballot(km[c] >= cand));
-        if (cnt >= k) {
-            thr = cand;
-            if (cnt == k) {  // exactly k keys reach thr: they are the top k
-                exact = true;
-                break;
-            }
-        }
-    }
-    unsigned long long chosen = 0;
-    if (exact) {
+        for (int c = 0; c < CPL; ++c) cnt += __popcll(bl[c]);
+        thi = cnt >= k ? cand : thi;
+        found = cnt == k;  // exactly k keys reach (thi, 0): they are the top k
+        bit >>= 1;
+    } while (!found && bit != 0u);
+    if (found) {
+        unsigned long long chosen = 0;
 #pragma unroll
         for (int c = 0; c < CPL; ++c)
-            if (km[c] >= thr) chosen |= 1ull << c;
+            if (hi[c] >= thi) chosen |= 1ull << c;
         return chosen;
     }
-    // thr is the k-th largest key; take all larger ones and the lowest-index ties.
+    // Low word, against the high word thi of the k-th largest key.
+    unsigned int l2[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) l2[c] = hi[c] > thi ? 0xffffffffu : (hi[c] == thi ? lo[c] : 0u);
+    unsigned int tlo = 0;
+    bit = 0x80000000u;
+    do {
+        const unsigned int cand = __builtin_amdgcn_readfirstlane(tlo | bit);
+        unsigned long long bl[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) bl[c] = __ballot(l2[c] >= cand);
+        int cnt = 0;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) cnt += __popcll(bl[c]);
+        tlo = cnt >= k ? cand : tlo;
+        found = cnt == k;
+        bit >>= 1;
+    } while (!found && bit != 0u);
+    if (found) {
+        unsigned long long chosen = 0;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+            if (l2[c] >= tlo) chosen |= 1ull << c;
+        return chosen;
+    }
+    // thr is the k-th largest key and is tied: take all larger keys and the
+    // lowest-index ties.
+    const unsigned long long thr = ((unsigned long long)thi << 32) | tlo;
+    unsigned long long km[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) km[c] = ((unsigned long long)hi[c] << 32) | lo[c];
     int gt = 0;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) gt += __popcll(__ballot(km[c] > thr));
     const int need = k - gt;
     int before = 0;
+    unsigned long long chosen = 0;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
         const bool tie = km[c] == thr;
@@ -250,14 +295,17 @@ struct SelCfg {
     static constexpr int CHK = chk();
     static constexpr int SROW = CHK * 64 + 2;          // doubles per staging row
     static constexpr int NCH = (CPL + CHK - 1) / CHK;  // chunks of slots
-    static_assert(2 * MT <= NW, "one weighted-sum item per wave at most");
+    // Key-block splits of the weighted sums: 2 MT KS items, one per wave; the KS
+    // partial tiles of a row sit side by side in its staging row.
+    static constexpr int KS = (NW / (2 * MT)) < CHK ? (NW / (2 * MT)) : CHK;
+    static_assert(KS >= 1, "one weighted-sum item per wave at most");
 };
 
 template <int CPL, int R, int NW>
 __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p)
 {
     using Cfg = SelCfg<CPL, R, NW>;
-    constexpr int RW = Cfg::RW, MT = Cfg::MT, CHK = Cfg::CHK, SROW = Cfg::SROW, NCH = Cfg::NCH;
+    constexpr int RW = Cfg::RW, MT = Cfg::MT, CHK = Cfg::CHK, SROW = Cfg::SROW, NCH = Cfg::NCH, KS = Cfg::KS;
     __shared__ __align__(16) double stage[16 * MT * SROW];
     __shared__ __align__(16) double wareas[NW * Cfg::WD];
     __shared__ float Ms[kD * (kD + 1)];
@@ -284,6 +332,7 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
         return wareas + (m / R) * Cfg::WD + (slot * R + m % R) * kD;
     };
     const int grp = lane >> 4, col = lane & 15;  // matrix-step lane coordinates
+    const WaveLds<R> lds{wareas + wave * Cfg::WD};
 
     // acc[r][c] = sum_d X_m[d] T_j[d] for this wave's rows m and key blocks
     // j = lane + 64 c, with X_m vector `xs` of row m and T the head's pooled tensor
@@ -300,8 +349,8 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
 #pragma unroll
         for (int q = 0; q < NCH; ++q) {
             const int t0 = 4 * CHK * q, t1 = min(4 * CHK * (q + 1), ntiles);
-            for (int t = t0 + (wave - t0 % NW + NW) % NW; t < t1; t += NW) {  // tile t: wave t mod NW
-                double b[16];
+            // Tile t belongs to wave t mod NW (loads past the tensor give zero).
+            auto load_b = [&](int t, double (&b)[16]) __attribute__((always_inline)) {
                 const int off = (16 * t + col) * kD * (int)sizeof(double) + grp * 128;
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
@@ -309,6 +358,10 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
                     b[2 * u] = v.x;
                     b[2 * u + 1] = v.y;
                 }
+            };
+            for (int t = t0 + (wave - t0 % NW + NW) % NW; t < t1; t += NW) {
+                double b[16];
+                load_b(t, b);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     v4d c = {0.0, 0.0, 0.0, 0.0};
@@ -335,15 +388,17 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     };
     // out_m[d] = sum_j w_m(j) Vbar_j[d] for every row m of the workgroup, into vector
     // `os` of row m, with w_m(j) = w[r][c] of the owning wave (zero for key blocks
-    // past n_kb). The owners stage their weights CHK slots at a time; item
-    // (mt, np) = (wave / 2, wave % 2) accumulates the 16 rows of tile mt against
-    // channels 32 np + 2 n + e (n < 16, e = 0, 1) over all key blocks: in each
-    // step the k index l / 16 stands for key block 8 o + 2 (l / 16) + (0 or 1) of
-    // the octet o, so that one 16-byte read gives the A values of two steps and
-    // one 16-byte read of a key block's channel pair the B values of two products.
+    // past n_kb). The owners stage their weights CHK slots at a time. Item
+    // (mt, np, ks) of wave mt 2 KS + np KS + ks accumulates the 16 rows of tile mt
+    // against channels 32 np + 2 n + e (n < 16, e = 0, 1) over the key-block
+    // octets o = ks (mod KS): in each step the k index l / 16 stands for key block
+    // 8 o + 2 (l / 16) + (0 or 1), so one 16-byte read gives the A values of two
+    // steps and one 16-byte read of a key block's channel pair the B values of two
+    // products. The KS partial tiles are then added in split order by the owners.
     auto wsum_pass = [&](const double (&w)[R][CPL], int os) __attribute__((always_inline)) {
-        const bool mine = wave < 2 * MT;
-        const int mt = wave >> 1, np = wave & 1;
+        const bool mine = wave < 2 * MT * KS;
+        const int it = mine ? wave : 0;
+        const int ks = it % KS, np = (it / KS) & 1, mt = it / (2 * KS);
         v4d c0 = {0.0, 0.0, 0.0, 0.0}, c1 = c0;
         const double *arow = stage + (16 * mt + col) * SROW + 2 * grp;
         const int boff = (32 * np + 2 * col) * (int)sizeof(double);
@@ -359,8 +414,8 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
             if (mine && kq > 0) {
                 const int noct = (kq + 7) >> 3;
                 const int key0 = 64 * CHK * q + 2 * grp;
-#pragma unroll 2
-                for (int o = 0; o < noct; ++o) {
+#pragma unroll 4
+                for (int o = ks; o < noct; o += KS) {
                     const double2 a = *reinterpret_cast<const double2 *>(arow + 8 * o);
                     const int key = key0 + 8 * o;
                     const double2 b0 = pooled_16(rsV, key * kD * (int)sizeof(double) + boff);
@@ -373,21 +428,26 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
             }
             __syncthreads();
         }
-        // c_e[v] = out[row 16 mt + 4 v + l / 16][channel 32 np + 2 (l % 16) + e]
+        // c_e[v] = partial of row 16 mt + 4 v + l / 16, channel 32 np + 2 (l % 16) + e
         if (mine) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int m = 16 * mt + 4 * v + grp;
-                if (m < RW) {
-                    double *o = row_vec(os, m) + 32 * np + 2 * col;
-                    *reinterpret_cast<double2 *>(o) = double2{c0[v], c1[v]};
-                }
+                double *o = stage + (16 * mt + 4 * v + grp) * SROW + ks * kD + 32 * np + 2 * col;
+                *reinterpret_cast<double2 *>(o) = double2{c0[v], c1[v]};
             }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const double *src = stage + (wave * R + r) * SROW + lane;
+            double tot = src[0];
+#pragma unroll
+            for (int k2 = 1; k2 < KS; ++k2) tot += src[k2 * kD];
+            lds.vec(os, r)[lane] = tot;
         }
         __syncthreads();
     };
 
-    const WaveLds<R> lds{wareas + wave * Cfg::WD};
     const double eps = p.eps;
     const double *cT = p.pooled.cT + (size_t)h * nkb;
     const int c_h = p.budgets[h];
