@@ -151,7 +151,7 @@ int ress_select(const ress_shape *shape, const ress_select_params *params, const
  * Arguments and results as ress_select; params->pooled_in_workspace must be 0
  * (RESS_E_INVALID_ARG otherwise); shapes whose workspace
  * (ress_select_workspace_size) exceeds RESS_NOALLOC_SCRATCH_BYTES return
- * RESS_E_UNSUPPORTED (the 100-view layer, 16 heads x 1074 blocks, needs 35 MB). */
+ * RESS_E_UNSUPPORTED (the 100-view layer, 16 heads x 1074 blocks, needs 26.5 MB). */
 #define RESS_NOALLOC_SCRATCH_BYTES (48u << 20)
 int ress_select_noalloc(const ress_shape *shape, const ress_select_params *params, const void *q, const void *k,
                         const void *v, const float *gram, const int32_t *keep_budget, int32_t *kept_count,

@@ -786,10 +786,11 @@ hipError_t launch_cfg(const SelectParams &p, hipStream_t s)
 // Rows per workgroup, among 24 (12 waves of 2 rows), 16 (8 waves of 2), 8 (8
 // waves of 1) and 4 (4 waves of 1): the one with the fewest rounds of
 // workgroups over the chip's 256 compute units (one workgroup each), weighted
-// by the rows each wave carries (its serial top-k work); ties go to more
-// workgroups. Two rows per wave only up to 6 slots per lane (their candidate
-// state must fit the registers of two or three waves per SIMD); 4 waves of 1
-// row beyond 1088 key blocks.
+// by the rows each wave carries (its serial top-k work); 4 rows over 8 on a tie
+// (more compute units busy), and 16 or 24 only when strictly cheaper. Two rows
+// per wave only up to 6 slots per lane (their candidate state must fit the
+// registers of two or three waves per SIMD); 4 waves of 1 row beyond 1088 key
+// blocks.
 constexpr long long kCUs = 256;
 template <int CPL, bool TWO_ROWS>
 hipError_t launch_rows(const SelectParams &p, hipStream_t s)
@@ -800,7 +801,7 @@ hipError_t launch_rows(const SelectParams &p, hipStream_t s)
     };
     int best = 8;
     long long bc = cost(8, 1);
-    if (cost(4, 1) < bc) best = 4, bc = cost(4, 1);
+    if (cost(4, 1) <= bc) best = 4, bc = cost(4, 1);
     if constexpr (TWO_ROWS) {
         if (cost(16, 2) < bc) best = 16, bc = cost(16, 2);
         if (cost(24, 2) < bc) best = 24, bc = cost(24, 2);

@@ -319,31 +319,39 @@ def test_config_layer_stack(ress, layer):
 
 
 def _launch_shape(H, n_qb, n_kb):
-    """Selection launch the library takes: slots per lane by key-block count, then
-    rows per workgroup 16 (8 waves of 2 rows, up to 384 key blocks), 8 (8 waves
-    of 1, up to 1088) or 4 (4 waves of 1), the most that still give each of the
-    256 compute units a workgroup."""
+    """Selection launch the library takes (the same rule, restated): slots per lane
+    by key-block count; then rows per workgroup among 8 (8 waves of 1 row), 4 (4
+    waves of 1), 16 (8 waves of 2) and 24 (12 waves of 2), by the fewest rounds of
+    workgroups over 256 compute units times (rows per wave + 1), 4 over 8 on a tie,
+    16 and 24 (only up to 384 key blocks) when strictly cheaper; 4 rows beyond 1088
+    key blocks."""
     for lim, cpl, two in ((128, 2, True), (256, 4, True), (384, 6, True), (512, 8, False), (768, 12, False),
                           (1088, 17, False), (2048, 32, None), (4096, 64, None)):
         if n_kb <= lim:
             break
     if two is None:
         return cpl, 4
-    wg = lambda rows: H * -(-n_qb // rows)
-    if two and wg(16) >= 256:
-        return cpl, 16
-    return (cpl, 8) if wg(8) >= 256 else (cpl, 4)
+    cost = lambda rows, r: -(-(H * -(-n_qb // rows)) // 256) * (r + 1)
+    best, bc = 8, cost(8, 1)
+    if cost(4, 1) <= bc:
+        best, bc = 4, cost(4, 1)
+    if two:
+        if cost(16, 2) < bc:
+            best, bc = 16, cost(16, 2)
+        if cost(24, 2) < bc:
+            best, bc = 24, cost(24, 2)
+    return cpl, best
 
 
 # (key blocks of 64 tokens, heads, slots per lane, rows per workgroup): every launch
 # shape of the selection.
-LAUNCH_SHAPES = [(120, 32, 2, 16), (120, 24, 2, 8), (120, 8, 2, 4),
-                 (200, 20, 4, 16), (200, 16, 4, 8), (200, 8, 4, 4),
-                 (350, 12, 6, 16), (350, 8, 6, 8), (350, 4, 6, 4),
-                 (450, 6, 8, 8), (450, 4, 8, 4),
-                 (700, 4, 12, 8), (700, 2, 12, 4),
-                 (1000, 4, 17, 8), (1000, 2, 17, 4),
-                 (1500, 2, 32, 4),
+LAUNCH_SHAPES = [(120, 33, 2, 24), (120, 18, 2, 16), (120, 9, 2, 8), (120, 1, 2, 4),
+                 (200, 20, 4, 24), (200, 11, 4, 16), (200, 6, 4, 8), (200, 1, 4, 4),
+                 (350, 12, 6, 24), (350, 6, 6, 16), (350, 3, 6, 8), (350, 1, 6, 4),
+                 (450, 3, 8, 8), (450, 1, 8, 4),
+                 (700, 2, 12, 8), (700, 1, 12, 4),
+                 (1000, 2, 17, 8), (1000, 1, 17, 4),
+                 (1500, 1, 32, 4),
                  (3000, 1, 64, 4)]
 
 
