@@ -39,10 +39,9 @@
 // logits are formed exactly; either way every score of a row has one form.
 // Softmax is invariant to the reference, so this changes rounding only.
 //
-// Workgroups are numbered so that each of the 8 XCDs runs a contiguous chunk of
-// query blocks of every head: neighbouring query blocks of a head share an XCD
-// and its L2, where their K/V tiles are re-read, and heads of different cost
-// (ragged budgets) are spread evenly over the XCDs.
+// Workgroups are numbered so that neighbouring query blocks of a head share an
+// XCD and its L2, where their K/V tiles are re-read, and heads of different cost
+// (ragged budgets) still split evenly over the XCDs (see row_of).
 #include <type_traits>
 
 #include "ress_internal.h"
@@ -77,6 +76,65 @@ __device__ __forceinline__ int swz(int row) { return (((row >> 1) & 1) << 2) | (
 
 __device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
+// Work order, two forms; within a head, last blocks first (the dense special
+// blocks early). Returns false for a workgroup with no row.
+//  - Segments (the K and V of all heads fit the infinity cache): the (head, query
+//    block) rows, head-major, are cut into 8 contiguous segments of about equal
+//    work, one per XCD, so that each XCD fills its L2 with few heads' K and V
+//    (neighbouring query blocks of a head share it) while ragged per-head budgets
+//    stay balanced. A row's work is its head's kept count of query block 0 (the
+//    rows of a head keep the same number of blocks, the dense special rows aside;
+//    dense attention: equal). Boundaries follow the work split, clamped so that no
+//    segment exceeds seg_cap rows (the grid is 8 x seg_cap workgroups; every row
+//    lands in exactly one segment).
+//  - Rotation (larger layers): XCD x runs, head after head, a chunk of seg_cap
+//    consecutive query blocks of every head, chunk (x - h) mod 8 of head h, so
+//    that each head's chunks are spread over all XCDs and the XCDs move through the
+//    heads together (the grid is 8 x H x seg_cap workgroups).
+__device__ __forceinline__ bool row_of(const AttnParams &p, bool sparse, int xcd, int local, int &h, int &i)
+{
+    const int H = p.H, n = p.n_qb;
+    if (p.rotate) {
+        const int chunk = p.seg_cap;
+        const int slot = local / chunk, r = local - slot * chunk;
+        if (slot >= H) return false;
+        h = (xcd + slot) % H;
+        const int i_fwd = ((xcd - h % 8 + 8) & 7) * chunk + r;
+        if (i_fwd >= n) return false;
+        i = n - 1 - i_fwd;
+        return true;
+    }
+    const long long T = (long long)H * n, cap = p.seg_cap;
+    auto weight = [&](int hh) -> long long {
+        return sparse ? (long long)max(p.kept_count[(size_t)hh * n], 1) : 1ll;
+    };
+    long long W = 0;
+    for (int hh = 0; hh < H; ++hh) W += weight(hh) * n;
+    // First row whose work prefix reaches x W / 8.
+    auto split = [&](int x) -> long long {
+        const long long target = (W / 8) * x + ((W % 8) * x + 7) / 8;
+        long long acc = 0;
+        for (int hh = 0; hh < H; ++hh) {
+            const long long w = weight(hh), seg = w * n;
+            if (acc + seg >= target)  // 0 < target - acc <= w n < 2^31
+                return (long long)hh * n + ((int)(target - acc) + (int)w - 1) / (int)w;
+            acc += seg;
+        }
+        return T;
+    };
+    long long b = 0, e = 0;
+    for (int x = 1; x <= xcd + 1; ++x) {
+        const long long lo = max(e, T - (8 - x) * cap), hi = min(e + cap, T);
+        b = e;
+        e = min(max(split(x), lo), hi);
+    }
+    const int g = (int)b + local;  // rows < 2^31 (checked on the host)
+    if (g >= (int)e) return false;
+    h = g / n;
+    i = n - 1 - (g - h * n);
+    return true;
+}
+
 template <int BQ, int BK, bool SPARSE>
 __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
 {
@@ -92,19 +150,9 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
     __shared__ __attribute__((aligned(1024))) unsigned char v_lds0[TILE];
     __shared__ __attribute__((aligned(1024))) unsigned char v_lds1[TILE];
 
-    // Work order: XCD x runs, head after head, one eighth of every head's query
-    // blocks (a contiguous chunk, so neighbouring query blocks share the XCD's L2),
-    // the chunk rotating with the head so that every XCD gets the same mix of heads
-    // (ragged per-head budgets stay balanced across XCDs) and the dense tail chunks
-    // of different heads land on different XCDs. Within a head, last blocks first.
     const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-    const int chunk = p.qb_chunk;
-    const int slot = local / chunk, r = local - slot * chunk;
-    if (slot >= p.H) return;
-    const int h = (xcd + slot) % p.H;
-    const int i_fwd = ((xcd - h % 8 + 8) & 7) * chunk + r;
-    if (i_fwd >= p.n_qb) return;
-    const int i = p.n_qb - 1 - i_fwd;
+    int h, i;
+    if (!row_of(p, SPARSE, xcd, local, h, i)) return;
     const int N = p.N, n_kb = p.n_kb;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -476,7 +524,7 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
 template <int BQ, int BK>
 hipError_t launch_bk(const AttnParams &p, bool sparse, hipStream_t s)
 {
-    const dim3 grid((unsigned)(8 * p.H * p.qb_chunk)), block(BQ * 2);
+    const dim3 grid((unsigned)(p.rotate ? 8 * p.H * p.seg_cap : 8 * p.seg_cap)), block(BQ * 2);
     if (sparse)
         hipLaunchKernelGGL((attn_kernel<BQ, BK, true>), grid, block, 0, s, p);
     else

@@ -352,14 +352,22 @@ static int attn_common(const ress_shape *shape, const void *q, const void *k, co
     if (o == q || o == k || o == v) return RESS_E_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return RESS_E_INVALID_ARG;
     if (sparse && (!kept_count || !kept_idx)) return RESS_E_INVALID_ARG;
-    const long long chunk = (g.n_qb + 7) / 8;
-    if (8 * chunk * shape->H > 0x7fffffffLL) return RESS_E_UNSUPPORTED;
+    // Work order (attn.hip): contiguous work-balanced segments per XCD while the
+    // K and V of all heads fit the 256 MB infinity cache, rotating per-head chunks
+    // beyond. Segments: up to 1.5 times an even share of rows per XCD, so that
+    // per-head work differing by up to that factor still splits evenly.
+    const long long rows = (long long)shape->H * g.n_qb;
+    const bool rotate = 2ll * shape->H * shape->N * kD * 2 > (256ll << 20);
+    const long long cap = rotate ? (g.n_qb + 7) / 8 : (3 * rows + 15) / 16;
+    const long long grid = rotate ? 8 * cap * shape->H : 8 * cap;
+    if (grid > 0x7fffffffLL) return RESS_E_UNSUPPORTED;
     ress::AttnParams ap;
     ap.H = shape->H;
     ap.N = shape->N;
     ap.n_qb = (int)g.n_qb;
     ap.n_kb = (int)g.n_kb;
-    ap.qb_chunk = (int)chunk;
+    ap.rotate = rotate ? 1 : 0;
+    ap.seg_cap = (int)cap;
     ap.scale_log2 = scale * 1.4426950408889634f;
     ap.q = static_cast<const uint16_t *>(q);
     ap.k = static_cast<const uint16_t *>(k);

@@ -46,7 +46,8 @@ struct SelectParams {
 
 struct AttnParams {
     int H, N, n_qb, n_kb;
-    int qb_chunk;       // query blocks per (head, XCD): ceil(n_qb / 8)
+    int rotate;         // work order: 0 work-balanced segments, 1 rotating chunks (see attn.hip)
+    int seg_cap;        // segments: most rows one XCD runs; rotation: query blocks per chunk
     float scale_log2;   // softmax scale * log2(e)
     const uint16_t *q, *k, *v;
     uint16_t *o;                           // bf16 output, unless o32 is set
