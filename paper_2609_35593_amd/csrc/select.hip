@@ -57,18 +57,117 @@ __device__ __forceinline__ double2 pooled_16(__amdgpu_buffer_rsrc_t rs, int off)
     return __builtin_bit_cast(double2, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
 }
 
+// Wave reductions on registers only (no LDS permutes): DPP exchanges within 16
+// lanes (lane i with i^1, i^2, then with 7-i within 8 and 15-i within 16, each
+// step adding a symmetric pair, so every lane holds the same partial), then the
+// gfx950 row swaps, whose two results added give x[l] + x[l^16] and
+// x[l] + x[l^32] in every lane. Commutative adds in a fixed pattern: the result
+// is identical in every lane and on every run.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x)
+{
+    const unsigned long long u = (unsigned long long)__double_as_longlong(x);
+    const int lo = __builtin_amdgcn_mov_dpp((int)(unsigned)u, CTRL, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(unsigned)(u >> 32), CTRL, 0xf, 0xf, false);
+    return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+// Lane l's value and that of lane l^16 (ROW32: l^32), in an order that is the
+// same for both lanes of the pair.
+template <bool ROW32>
+__device__ __forceinline__ void swap_pair(double x, double &d0, double &d1)
+{
+    const unsigned long long u = (unsigned long long)__double_as_longlong(x);
+    const unsigned lo = (unsigned)u, hi = (unsigned)(u >> 32);
+    const auto a = ROW32 ? __builtin_amdgcn_permlane32_swap(lo, lo, false, false)
+                         : __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto b = ROW32 ? __builtin_amdgcn_permlane32_swap(hi, hi, false, false)
+                         : __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    d0 = __longlong_as_double((long long)(((unsigned long long)b[0] << 32) | a[0]));
+    d1 = __longlong_as_double((long long)(((unsigned long long)b[1] << 32) | a[1]));
+}
+
+template <bool ROW32>
+__device__ __forceinline__ double swap_sum(double x)
+{
+    double d0, d1;
+    swap_pair<ROW32>(x, d0, d1);
+    return d0 + d1;
+}
+
 __device__ __forceinline__ double wave_sum(double x)
 {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
-    return x;  // butterfly with commutative adds: identical in every lane
+    x += dpp_f64<0xB1>(x);   // quad_perm [1,0,3,2]: lane i^1
+    x += dpp_f64<0x4E>(x);   // quad_perm [2,3,0,1]: lane i^2
+    x += dpp_f64<0x141>(x);  // row_half_mirror: lane 7-i within 8
+    x += dpp_f64<0x140>(x);  // row_mirror: lane 15-i within 16
+    x = swap_sum<false>(x);  // + the partner 16-lane row
+    return swap_sum<true>(x);  // + the other 32 lanes
+}
+
+// Two wave sums with their exchanges interleaved.
+__device__ __forceinline__ void wave_sum2(double a, double b, double &sa, double &sb)
+{
+    a += dpp_f64<0xB1>(a);
+    b += dpp_f64<0xB1>(b);
+    a += dpp_f64<0x4E>(a);
+    b += dpp_f64<0x4E>(b);
+    a += dpp_f64<0x141>(a);
+    b += dpp_f64<0x141>(b);
+    a += dpp_f64<0x140>(a);
+    b += dpp_f64<0x140>(b);
+    a = swap_sum<false>(a);
+    b = swap_sum<false>(b);
+    sa = swap_sum<true>(a);
+    sb = swap_sum<true>(b);
+}
+
+template <int CTRL>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long u)
+{
+    const int lo = __builtin_amdgcn_mov_dpp((int)(unsigned)u, CTRL, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(unsigned)(u >> 32), CTRL, 0xf, 0xf, false);
+    return ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo;
+}
+
+template <bool ROW32>
+__device__ __forceinline__ unsigned long long swap_max_u64(unsigned long long u)
+{
+    const unsigned lo = (unsigned)u, hi = (unsigned)(u >> 32);
+    const auto a = ROW32 ? __builtin_amdgcn_permlane32_swap(lo, lo, false, false)
+                         : __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto b = ROW32 ? __builtin_amdgcn_permlane32_swap(hi, hi, false, false)
+                         : __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    const unsigned long long d0 = ((unsigned long long)b[0] << 32) | a[0];
+    const unsigned long long d1 = ((unsigned long long)b[1] << 32) | a[1];
+    return d0 > d1 ? d0 : d1;
+}
+
+// Largest 64-bit unsigned value over the wave, in every lane.
+__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long x)
+{
+    unsigned long long y = dpp_u64<0xB1>(x);
+    x = y > x ? y : x;
+    y = dpp_u64<0x4E>(x);
+    x = y > x ? y : x;
+    y = dpp_u64<0x141>(x);
+    x = y > x ? y : x;
+    y = dpp_u64<0x140>(x);
+    x = y > x ? y : x;
+    return swap_max_u64<true>(swap_max_u64<false>(x));
 }
 
 __device__ __forceinline__ double wave_max(double x)
 {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) x = fmax(x, __shfl_xor(x, o));
-    return x;
+    x = fmax(x, dpp_f64<0xB1>(x));
+    x = fmax(x, dpp_f64<0x4E>(x));
+    x = fmax(x, dpp_f64<0x141>(x));
+    x = fmax(x, dpp_f64<0x140>(x));
+    double d0, d1;
+    swap_pair<false>(x, d0, d1);
+    x = fmax(d0, d1);
+    swap_pair<true>(x, d0, d1);
+    return fmax(d0, d1);
 }
 
 __device__ __forceinline__ v4d mfma_f64(double a, double b, v4d c)
@@ -198,11 +297,7 @@ __device__ __forceinline__ unsigned long long topk_small(const unsigned long lon
             const unsigned long long v = ((left >> c) & 1ull) ? key[c] : 0ull;
             best = v > best ? v : best;
         }
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const unsigned long long other = __shfl_xor(best, o);
-            best = other > best ? other : best;
-        }
+        best = wave_max_u64(best);
         // best > 0: at least one member is left (k <= members)
         bool done = false;
 #pragma unroll
@@ -624,14 +719,16 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     double *hv[R];  // M g reuses the slot of S vbar
 #pragma unroll
     for (int r = 0; r < R; ++r) hv[r] = wvv[r];
-    auto objective = [&]() {  // h = M g, G = g . h, J = G / max(K, eps)^2
+    // h = M g, G = g . h, J = G / max(K, eps)^2, and vbar . h for the next round's gains.
+    double vmg[R];
+    auto objective = [&]() {
         __builtin_amdgcn_wave_barrier();
         double hh[R];
         mat_vec<R, false>(Ms, gv, hh, lane);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             hv[r][lane] = hh[r];
-            G[r] = wave_sum(gv[r][lane] * hh[r]);
+            wave_sum2(gv[r][lane] * hh[r], vbv[r][lane] * hh[r], G[r], vmg[r]);
             const double Kh = K[r] > eps ? K[r] : eps;
             J[r] = G[r] / (Kh * Kh);
         }
@@ -661,11 +758,9 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
         // e_k . (M g) = vbar . (M g) - Vbar_k . (M g) for every candidate k of every row.
         dot_pass(1, rsV, acc);
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const double vmg = wave_sum(vbv[r][lane] * hv[r][lane]);
+        for (int r = 0; r < R; ++r)
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) acc[r][c] = vmg - acc[r][c];
-        }
+            for (int c = 0; c < CPL; ++c) acc[r][c] = vmg[r] - acc[r][c];
         // Gains of every single restore / drop at the round-start state; the m best
         // of each kind are applied together, g and K following Eq. 13.
 #pragma unroll
@@ -735,7 +830,7 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
                 nbuf += n;
             }
             if (nbuf > 0) apply();
-            K[r] = (K[r] + wave_sum(mr)) - wave_sum(md);
+            K[r] += wave_sum(mr - md);
             __builtin_amdgcn_wave_barrier();
             gv[r][lane] = g;
         }
