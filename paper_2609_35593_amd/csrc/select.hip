@@ -183,21 +183,66 @@ __device__ __forceinline__ unsigned long long order_key(double x)
     return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
+// Bitwise search over member high words h[0..NS) (zero for non-members): the
+// largest t such that at least k of them reach t with a zero low word below it,
+// built bit by bit; found = exactly k reach it. The threshold, bit and counts are
+// wave-uniform and the loop has a single exit, so that it runs on scalar
+// registers and scalar branches.
+template <int NS>
+__device__ __forceinline__ unsigned int search_high(const unsigned int (&h)[NS], int k, int &found)
+{
+    unsigned int thi = 0, bit = 0x80000000u;
+    do {
+        const unsigned int cand = __builtin_amdgcn_readfirstlane(thi | bit);
+        unsigned long long bl[NS];
+#pragma unroll
+        for (int c = 0; c < NS; ++c) bl[c] = __ballot(h[c] >= cand);
+        int cnt = 0;
+#pragma unroll
+        for (int c = 0; c < NS; ++c) cnt += __popcll(bl[c]);
+        thi = cnt >= k ? cand : thi;
+        found = cnt == k;
+        bit >>= 1;
+    } while (!found && bit != 0u);
+    return thi;
+}
+
+// The member high words packed into the first NS slots (zero past them) through
+// the wave's scratch scr (this wave's LDS only), when at most 64 NS are members.
+template <int CPL, int NS>
+__device__ __forceinline__ void pack_high(const unsigned int (&hi)[CPL], unsigned long long mbits, int nmem,
+                                          unsigned int *scr, unsigned long long lane_lt, int lane,
+                                          unsigned int (&h)[NS])
+{
+    int base = 0;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+        const bool m = (mbits >> c) & 1ull;
+        const unsigned long long bl = __ballot(m);
+        if (m) scr[base + __popcll(bl & lane_lt)] = hi[c];
+        base += __popcll(bl);
+    }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int c = 0; c < NS; ++c) h[c] = 64 * c + lane < nmem ? scr[64 * c + lane] : 0u;
+    __builtin_amdgcn_wave_barrier();
+}
+
 // Exact top-k of the member slots by (key desc, block index asc). Bit c of
 // mbits marks this lane's slot c as a member. Non-member keys are replaced by 0,
 // below every member key (an order key of a finite value is at least 1), so one
 // ballot per slot counts members only. The k-th largest key is found bit by
-// bit, high word first: while the low word of a candidate threshold is zero, a
-// key reaches it exactly when its high word does. Once the high word t of the
-// k-th largest key is known, a key reaches a candidate (t, x) (x >= 1) exactly
-// when the 32-bit value "all ones if its high word is above t, its low word if
-// equal, zero if below" reaches x. Every count is wave-uniform (scalar
-// registers); the search stops as soon as exactly k keys reach the threshold.
-// Returns this lane's chosen slots as a bit mask. Requires 0 <= k <= number of
-// members.
+// bit, high word first (search_high); when the members fit 2 or 4 slots and a
+// scratch is given, that search runs on them packed (same threshold, fewer
+// compares). Once the high word t of the k-th largest key is known, a key
+// reaches a candidate (t, x) (x >= 1) exactly when the 32-bit value "all ones if
+// its high word is above t, its low word if equal, zero if below" reaches x. The
+// search stops as soon as exactly k keys reach the threshold. Returns this
+// lane's chosen slots as a bit mask. Requires 0 <= k <= number of members.
 template <int CPL>
 __device__ __forceinline__ unsigned long long topk_slots(const unsigned long long (&key)[CPL],
-                                                         unsigned long long mbits, int k, unsigned long long lane_lt)
+                                                         unsigned long long mbits, int k, unsigned long long lane_lt,
+                                                         unsigned int *scr = nullptr, int lane = 0)
 {
     k = __builtin_amdgcn_readfirstlane(k);
     if (k <= 0) return 0ull;
@@ -208,24 +253,26 @@ __device__ __forceinline__ unsigned long long topk_slots(const unsigned long lon
         hi[c] = (unsigned int)(km >> 32);
         lo[c] = (unsigned int)km;
     }
-    // High word: invariant #members with high word >= thi is >= k. The
-    // threshold, the bit and the counts are wave-uniform and the loop has a
-    // single exit, so that it runs on scalar registers and scalar branches.
-    unsigned int thi = 0, bit = 0x80000000u;
     int found = 0;
-    do {
-        const unsigned int cand = __builtin_amdgcn_readfirstlane(thi | bit);
-        unsigned long long bl[CPL];
+    unsigned int thi;
+    int nmem = 64 * CPL;
+    if (scr != nullptr && CPL > 2) {
+        nmem = 0;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) bl[c] = __ballot(hi[c] >= cand);
-        int cnt = 0;
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) cnt += __popcll(bl[c]);
-        thi = cnt >= k ? cand : thi;
-        found = cnt == k;  // exactly k keys reach (thi, 0): they are the top k
-        bit >>= 1;
-    } while (!found && bit != 0u);
-    if (found) {
+        for (int c = 0; c < CPL; ++c) nmem += __popcll(__ballot((mbits >> c) & 1ull));
+    }
+    if (CPL > 2 && nmem <= 128) {
+        unsigned int h[2];
+        pack_high<CPL, 2>(hi, mbits, nmem, scr, lane_lt, lane, h);
+        thi = search_high<2>(h, k, found);
+    } else if (CPL > 4 && nmem <= 256) {
+        unsigned int h[4];
+        pack_high<CPL, 4>(hi, mbits, nmem, scr, lane_lt, lane, h);
+        thi = search_high<4>(h, k, found);
+    } else {
+        thi = search_high<CPL>(hi, k, found);
+    }
+    if (found) {  // exactly k keys reach (thi, 0): they are the top k
         unsigned long long chosen = 0;
 #pragma unroll
         for (int c = 0; c < CPL; ++c)
@@ -236,8 +283,7 @@ __device__ __forceinline__ unsigned long long topk_slots(const unsigned long lon
     unsigned int l2[CPL];
 #pragma unroll
     for (int c = 0; c < CPL; ++c) l2[c] = hi[c] > thi ? 0xffffffffu : (hi[c] == thi ? lo[c] : 0u);
-    unsigned int tlo = 0;
-    bit = 0x80000000u;
+    unsigned int tlo = 0, bit = 0x80000000u;
     do {
         const unsigned int cand = __builtin_amdgcn_readfirstlane(tlo | bit);
         unsigned long long bl[CPL];
@@ -316,13 +362,14 @@ __device__ __forceinline__ unsigned long long topk_small(const unsigned long lon
 }
 
 // Top-k of the member slots: extraction for k up to 2, bitwise search beyond
-// (measured: extraction costs more than the search from k = 5 on).
+// (measured: extraction costs more than the search from k = 5 on); scr as for
+// topk_slots.
 template <int CPL>
 __device__ __forceinline__ unsigned long long topk_any(const unsigned long long (&key)[CPL],
                                                        unsigned long long mbits, int k, int lane,
-                                                       unsigned long long lane_lt)
+                                                       unsigned long long lane_lt, unsigned int *scr)
 {
-    return k <= 2 ? topk_small<CPL>(key, mbits, k, lane) : topk_slots<CPL>(key, mbits, k, lane_lt);
+    return k <= 2 ? topk_small<CPL>(key, mbits, k, lane) : topk_slots<CPL>(key, mbits, k, lane_lt, scr, lane);
 }
 
 // Swap count of round r (Eq. 17): max(floor, floor(rho c 2^-(r+1))).
@@ -746,6 +793,9 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     // swaps anything.
     double *swap_w = lds.swap_w();
     int *swap_j = lds.swap_j();
+    // The wave's own staging rows, idle between the products: scratch for packing
+    // sparse member sets in the searches.
+    unsigned int *scr = reinterpret_cast<unsigned int *>(stage + (size_t)wave * R * SROW);
     for (int rr = 0; rr < p.rounds; ++rr) {
         int mrow[R], mmax = 0;
 #pragma unroll
@@ -778,8 +828,8 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
                 const double dJ = J[r] - (G[r] + dG) / (Knh * Knh);  // Eq. 16
                 dj[c] = order_key(maximise ? -dJ : dJ);
             }
-            const unsigned long long rest = topk_any<CPL>(dj, inD[r], m, lane, lane_lt);
-            const unsigned long long drop = topk_any<CPL>(dj, cand_bits & ~inD[r], m, lane, lane_lt);
+            const unsigned long long rest = topk_any<CPL>(dj, inD[r], m, lane, lane_lt, scr);
+            const unsigned long long drop = topk_any<CPL>(dj, cand_bits & ~inD[r], m, lane, lane_lt, scr);
             inD[r] = (inD[r] & ~rest) | drop;
             double mr = 0.0, md = 0.0;
             double g = gv[r][lane];
