@@ -394,30 +394,6 @@ struct WaveLds {
     __device__ int *swap_j() const { return reinterpret_cast<int *>(base + kVecs * R * kD + kSwaps); }
 };
 
-// x_r = M y_r for the R rows, lane <-> output channel, M row-major in LDS (padded
-// rows), y_r broadcast from LDS two channels at a time; with SYM, x_r = (M + M^T)/2
-// y_r (the matrix whose quadratic form equals that of M, exact in float64 from
-// float32 entries).
-template <int R, bool SYM>
-__device__ __forceinline__ void mat_vec(const float *Ms, double *const (&y)[R], double (&x)[R], int lane)
-{
-#pragma unroll
-    for (int r = 0; r < R; ++r) x[r] = 0.0;
-#pragma unroll 4
-    for (int b = 0; b < kD; b += 2) {
-        double m0 = (double)Ms[lane * (kD + 1) + b], m1 = (double)Ms[lane * (kD + 1) + b + 1];
-        if (SYM) {
-            m0 = 0.5 * (m0 + (double)Ms[b * (kD + 1) + lane]);
-            m1 = 0.5 * (m1 + (double)Ms[(b + 1) * (kD + 1) + lane]);
-        }
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const double2 yb = *reinterpret_cast<const double2 *>(y[r] + b);
-            x[r] = fma(m1, yb.y, fma(m0, yb.x, x[r]));
-        }
-    }
-}
-
 // Sizes of a workgroup configuration: RW rows in MT 16-row tiles; the LDS
 // staging area holds 16 MT rows of CHK slots (64 key blocks each) plus 2 doubles
 // of padding per row (so that rows start on different 16-byte bank groups), as
@@ -441,6 +417,7 @@ struct SelCfg {
     // partial tiles of a row sit side by side in its staging row.
     static constexpr int KS = (NW / (2 * MT)) < CHK ? (NW / (2 * MT)) : CHK;
     static_assert(KS >= 1, "one weighted-sum item per wave at most");
+    static_assert(4 * MT <= NW, "one mat-vec item per wave at most");
 };
 
 template <int CPL, int R, int NW>
@@ -590,6 +567,43 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
         __syncthreads();
     };
 
+    // x_m = A y_m for every row m of the workgroup (y: vector `ys`, x: vector `xs`)
+    // with A = M_h, or with SYM its symmetric part (M + M^T) / 2 (the same quadratic
+    // form; exact in float64 from float32 entries). Item (mt, nt) of 4 MT, on
+    // wave mt 4 + nt: the 16 rows of tile mt against output channels 16 nt .. +15,
+    // k <-> channel 16 (l / 16) + s in step s as in dot_pass; B from M_h in LDS.
+    // Ends with a workgroup barrier (the owners then read x).
+    auto mv_pass = [&](auto sym, int ys, int xs) __attribute__((always_inline)) {
+        constexpr bool SYM = decltype(sym)::value;
+        if (wave < 4 * MT) {
+            const int mt = wave >> 2, nt = wave & 3;
+            const double *arow = row_vec(ys, min(16 * mt + col, RW - 1)) + 16 * grp;
+            const int n = 16 * nt + col;
+            v4d c = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const double2 a = *reinterpret_cast<const double2 *>(arow + 2 * u);
+                const int k = 16 * grp + 2 * u;
+                double b0 = (double)Ms[n * (kD + 1) + k], b1 = (double)Ms[n * (kD + 1) + k + 1];
+                if (SYM) {
+                    b0 = 0.5 * (b0 + (double)Ms[k * (kD + 1) + n]);
+                    b1 = 0.5 * (b1 + (double)Ms[(k + 1) * (kD + 1) + n]);
+                }
+                c = mfma_f64(a.x, b0, c);
+                c = mfma_f64(a.y, b1, c);
+            }
+            // c[v] = x[row 16 mt + 4 v + l / 16][channel n]
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int m = 16 * mt + 4 * v + grp;
+                if (m < RW) row_vec(xs, m)[n] = c[v];
+            }
+        }
+        __syncthreads();
+    };
+    using plain_mv = std::integral_constant<bool, false>;
+    using sym_mv = std::integral_constant<bool, true>;
+
     const double eps = p.eps;
     const double *cT = p.pooled.cT + (size_t)h * nkb;
     const int c_h = p.budgets[h];
@@ -656,15 +670,9 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     double vsv[R];
     {
         wsum_pass(P, 0);
-        double vb[R], wv[R];
-        mat_vec<R, true>(Ms, vbv, wv, lane);
+        mv_pass(sym_mv{}, 0, 1);  // every row's w in place
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            vb[r] = vbv[r][lane];
-            wvv[r][lane] = wv[r];
-            vsv[r] = wave_sum(vb[r] * wv[r]);
-        }
-        __syncthreads();  // every row's w in place
+        for (int r = 0; r < R; ++r) vsv[r] = wave_sum(vbv[r][lane] * wvv[r][lane]);
     }
 
     // q_ij = e^T M e with e = vbar_i - Vbar_j (Eq. 9), expanded through the symmetric
@@ -769,17 +777,15 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
     // h = M g, G = g . h, J = G / max(K, eps)^2, and vbar . h for the next round's gains.
     double vmg[R];
     auto objective = [&]() {
-        __builtin_amdgcn_wave_barrier();
-        double hh[R];
-        mat_vec<R, false>(Ms, gv, hh, lane);
+        __syncthreads();  // every row's g in place
+        mv_pass(plain_mv{}, 2, 1);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            hv[r][lane] = hh[r];
-            wave_sum2(gv[r][lane] * hh[r], vbv[r][lane] * hh[r], G[r], vmg[r]);
+            const double hh = hv[r][lane];
+            wave_sum2(gv[r][lane] * hh, vbv[r][lane] * hh, G[r], vmg[r]);
             const double Kh = K[r] > eps ? K[r] : eps;
             J[r] = G[r] / (Kh * Kh);
         }
-        __builtin_amdgcn_wave_barrier();
     };
     objective();
 #pragma unroll
