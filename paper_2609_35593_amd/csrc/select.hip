@@ -934,16 +934,16 @@ hipError_t launch_cfg(const SelectParams &p, hipStream_t s)
     return hipGetLastError();
 }
 
-// Rows per workgroup, among 24 (12 waves of 2 rows), 16 (8 waves of 2), 8 (8
+// Rows per workgroup, among 24 (8 waves of 3 rows), 16 (8 waves of 2), 8 (8
 // waves of 1) and 4 (4 waves of 1): the one with the fewest rounds of
 // workgroups over the chip's 256 compute units (one workgroup each), weighted
-// by the rows each wave carries (its serial top-k work); 4 rows over 8 on a tie
-// (more compute units busy), and 16 or 24 only when strictly cheaper. Two rows
-// per wave only up to 6 slots per lane (their candidate state must fit the
-// registers of two or three waves per SIMD); 4 waves of 1 row beyond 1088 key
+// by the rows each wave carries plus one (its serial row work); 4 rows over 8
+// on a tie (more compute units busy), and 16 or 24 only when strictly cheaper.
+// Several rows per wave only up to 6 slots per lane (their candidate state must
+// fit the registers of two waves per SIMD); 4 waves of 1 row beyond 1088 key
 // blocks.
 constexpr long long kCUs = 256;
-template <int CPL, bool TWO_ROWS>
+template <int CPL, bool MULTI_ROW>
 hipError_t launch_rows(const SelectParams &p, hipStream_t s)
 {
     auto cost = [&](int rows, int r) {
@@ -953,12 +953,10 @@ hipError_t launch_rows(const SelectParams &p, hipStream_t s)
     int best = 8;
     long long bc = cost(8, 1);
     if (cost(4, 1) <= bc) best = 4, bc = cost(4, 1);
-    if constexpr (TWO_ROWS) {
+    if constexpr (MULTI_ROW) {
         if (cost(16, 2) < bc) best = 16, bc = cost(16, 2);
-        if (cost(24, 2) < bc) best = 24, bc = cost(24, 2);
-    }
-    if constexpr (TWO_ROWS) {
-        if (best == 24) return launch_cfg<CPL, 2, 12>(p, s);
+        if (cost(24, 3) < bc) best = 24, bc = cost(24, 3);
+        if (best == 24) return launch_cfg<CPL, 3, 8>(p, s);
         if (best == 16) return launch_cfg<CPL, 2, 8>(p, s);
     }
     if (best == 8) return launch_cfg<CPL, 1, 8>(p, s);

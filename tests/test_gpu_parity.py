@@ -321,7 +321,7 @@ def test_config_layer_stack(ress, layer):
 def _launch_shape(H, n_qb, n_kb):
     """Selection launch the library takes (the same rule, restated): slots per lane
     by key-block count; then rows per workgroup among 8 (8 waves of 1 row), 4 (4
-    waves of 1), 16 (8 waves of 2) and 24 (12 waves of 2), by the fewest rounds of
+    waves of 1), 16 (8 waves of 2) and 24 (8 waves of 3), by the fewest rounds of
     workgroups over 256 compute units times (rows per wave + 1), 4 over 8 on a tie,
     16 and 24 (only up to 384 key blocks) when strictly cheaper; 4 rows beyond 1088
     key blocks."""
@@ -338,15 +338,15 @@ def _launch_shape(H, n_qb, n_kb):
     if two:
         if cost(16, 2) < bc:
             best, bc = 16, cost(16, 2)
-        if cost(24, 2) < bc:
-            best, bc = 24, cost(24, 2)
+        if cost(24, 3) < bc:
+            best, bc = 24, cost(24, 3)
     return cpl, best
 
 
 # (key blocks of 64 tokens, heads, slots per lane, rows per workgroup): every launch
 # shape of the selection.
-LAUNCH_SHAPES = [(120, 33, 2, 24), (120, 18, 2, 16), (120, 9, 2, 8), (120, 1, 2, 4),
-                 (200, 20, 4, 24), (200, 11, 4, 16), (200, 6, 4, 8), (200, 1, 4, 4),
+LAUNCH_SHAPES = [(120, 35, 2, 24), (120, 18, 2, 16), (120, 9, 2, 8), (120, 1, 2, 4),
+                 (200, 21, 4, 24), (200, 11, 4, 16), (200, 6, 4, 8), (200, 1, 4, 4),
                  (350, 12, 6, 24), (350, 6, 6, 16), (350, 3, 6, 8), (350, 1, 6, 4),
                  (450, 3, 8, 8), (450, 1, 8, 4),
                  (700, 2, 12, 8), (700, 1, 12, 4),
