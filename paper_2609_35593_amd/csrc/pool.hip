@@ -44,13 +44,17 @@ __device__ __forceinline__ double wave_block_mean(const uint16_t *__restrict__ x
 {
     const int lane = threadIdx.x & 63, chunk = lane >> 3, sub = lane & 7;
     double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    // All 16 loads are issued unconditionally (tokens past the block's end read its
+    // last token, cnt >= 1) and zeroed afterwards, so that a wave has its whole
+    // block in flight at once.
+    const uint16_t *base = x + row0 * kD + chunk * 8;
     uint4 w[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int tok = sub + 8 * r;
-        w[r] = tok < cnt ? *reinterpret_cast<const uint4 *>(x + (row0 + tok) * kD + chunk * 8)
-                         : make_uint4(0, 0, 0, 0);
-    }
+    for (int r = 0; r < 16; ++r)
+        w[r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(sub + 8 * r, cnt - 1) * kD);
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+        if (sub + 8 * r >= cnt) w[r] = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int r = 0; r < 16; ++r) accum_bf16x8(acc, w[r]);
 #pragma unroll

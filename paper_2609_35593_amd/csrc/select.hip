@@ -328,7 +328,7 @@ __device__ __forceinline__ unsigned long long topk_slots(const unsigned long lon
 
 // The same selection as topk_slots for small k, by k extractions of the largest
 // remaining member key: per lane the largest over its slots (lowest slot on
-// ties), then over the wave (a butterfly), then the lowest block index among
+// ties), then over the wave (wave_max_u64), then the lowest block index among
 // the slots holding that key (slots in ascending order, lanes in ascending
 // order within a slot, which is ascending block index).
 template <int CPL>
