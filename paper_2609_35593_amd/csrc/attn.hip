@@ -320,13 +320,16 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
                     acc_o[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t][u], acc_o[dh], 0, 0, 0);
                 }
     };
+    // Key of element (t, v) of a half: t 32 + (v / 4) 8 + (v % 4) + 4 hh; compared as
+    // 4 hh >= nv - (the lane-independent part), a scalar per element.
+    const int hh4 = hh * 4;
     auto mask = [&](f32x16 (&s)[2], int nv) __attribute__((always_inline)) {
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int key = t * 32 + (v >> 2) * 8 + hh * 4 + (v & 3);
-                if (key >= nv) s[t][v] = -INFINITY;
+                const int lim = __builtin_amdgcn_readfirstlane(nv - (t * 32 + (v >> 2) * 8 + (v & 3)));
+                if (hh4 >= lim) s[t][v] = -INFINITY;
             }
     };
     // Probabilities of sub-tile t (32 keys) of a half, exp2(s) when every row has
