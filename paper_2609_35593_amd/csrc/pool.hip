@@ -17,6 +17,8 @@
 namespace ress {
 namespace {
 
+typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
+
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;  // blocks per workgroup
 
@@ -46,12 +48,15 @@ __device__ __forceinline__ double wave_block_mean(const uint16_t *__restrict__ x
     double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     // All 16 loads are issued unconditionally (tokens past the block's end read its
     // last token, cnt >= 1) and zeroed afterwards, so that a wave has its whole
-    // block in flight at once.
+    // block in flight at once. Q, K and V are read once here: non-temporal loads,
+    // which leave the caches' resident lines in place (measured: with the caches
+    // full of dirty lines, the pass takes ~45 us less at 32 views).
     const uint16_t *base = x + row0 * kD + chunk * 8;
     uint4 w[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r)
-        w[r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(sub + 8 * r, cnt - 1) * kD);
+        w[r] = __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const v4u32 *>(
+                                             base + (size_t)min(sub + 8 * r, cnt - 1) * kD)));
 #pragma unroll
     for (int r = 0; r < 16; ++r)
         if (sub + 8 * r >= cnt) w[r] = make_uint4(0, 0, 0, 0);
