@@ -377,19 +377,23 @@ __global__ void __launch_bounds__(BQ * 2, 2) attn_kernel(const AttnParams p)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) tmax = fmaxf(tmax, s[t][v]);
             tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * cw;
+            // Decisions about the row's mass use the row's running sum: lanes l and
+            // l^32 each sum half of the row's keys (one of them may have no mass yet
+            // while the row has), and both must take the same reference.
+            const float lsum = lrow + __shfl_xor(lrow, 32);
             // The reference only rises, except while the row has no usable mass yet:
             // then it may fall to this half's maximum, but not below
-            // mref + log2(lrow), an upper bound of every earlier logit of the row, so
-            // that the rescaled running sum stays at most 1 (finite).
+            // mref + log2(lsum), an upper bound of every earlier logit of the row, so
+            // that the rescaled running sums stay at most 1 (finite).
             float mnew = fmaxf(mref, tmax);
             // (log2 of a denormal sum may come back as -inf: -149 bounds it.)
-            if (lrow < kTiny) mnew = lrow > 0.f ? fmaxf(tmax, mref + fmaxf(__log2f(lrow), -149.f)) : tmax;
+            if (lsum < kTiny) mnew = lsum > 0.f ? fmaxf(tmax, mref + fmaxf(__log2f(lsum), -149.f)) : tmax;
             if (tmax == -INFINITY) mnew = mref;  // a fully masked half says nothing
             if (fabsf(mnew) <= kZeroBand) mnew = 0.f;
             // A row without mass has nothing to rescale (and 0 * exp2(large) must not
             // happen); otherwise the factor is applied as two halves, each finite
             // for shifts up to 2^8 (a running sum as small as the smallest denormal).
-            const float alpha = lrow > 0.f ? __builtin_amdgcn_exp2f(0.5f * (mref - mnew)) : 0.f;
+            const float alpha = lsum > 0.f ? __builtin_amdgcn_exp2f(0.5f * (mref - mnew)) : 0.f;
             lrow = (lrow * alpha) * alpha;
 #pragma unroll
             for (int dh = 0; dh < 2; ++dh)
