@@ -683,11 +683,43 @@ __global__ void __launch_bounds__(NW * 64, 1) select_kernel(const SelectParams p
 #pragma unroll
     for (int c = 0; c < CPL; ++c) cj[c] = cT[jc[c]];
     dot_pass(1, rsV, acc);
+    // The block with P > 1/2, if a row has one (at most one does): there e = vbar_i -
+    // Vbar_j shrinks with 1 - P while the expansion's terms do not, so the expansion
+    // would leave mostly rounding error (a single-block row: e = 0 exactly). Its q is
+    // taken directly as e^T M e (M_h from LDS; e through the wave's staging rows, idle
+    // after the product): lane t forms e_t (M e)_t.
+    int dom_c[R], dom_l[R];
+    double q_dom[R];
+    {
+        double *ebuf = stage + (size_t)wave * R * SROW;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            dom_c[r] = -1;
+            dom_l[r] = 0;
+            q_dom[r] = 0.0;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                const unsigned long long b = __ballot(valid[c] && P[r][c] > 0.5);
+                if (b != 0ull) {
+                    dom_c[r] = c;
+                    dom_l[r] = __builtin_ctzll(b);
+                }
+            }
+            if (dom_c[r] < 0) continue;
+            const double e = vbv[r][lane] - pooled_row(rsV, dom_l[r] + 64 * dom_c[r], lane);
+            ebuf[lane] = e;
+            __builtin_amdgcn_wave_barrier();
+            double u = 0.0;
+            for (int c = 0; c < kD; ++c) u = fma((double)Ms[lane * (kD + 1) + c], ebuf[c], u);
+            __builtin_amdgcn_wave_barrier();
+            q_dom[r] = wave_sum(e * u);
+        }
+    }
 #pragma unroll
     for (int r = 0; r < R; ++r) {
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-            const double q = fma(-2.0, acc[r][c], vsv[r] + cj[c]);
+            const double q = (c == dom_c[r] && lane == dom_l[r]) ? q_dom[r] : fma(-2.0, acc[r][c], vsv[r] + cj[c]);
             const double s = P[r][c] * sqrt(q > 0.0 ? q : 0.0);
             const double den = 1.0 - P[r][c];
             S2[r][c] = s * s;
