@@ -525,3 +525,36 @@ def test_key_block_cap(ress, bq, bk):
     rng = np.random.default_rng(bk)
     rows = np.unique(np.concatenate([rng.integers(0, L.n_qb, 1000), [0, 1, L.n_qb // 2, L.n_qb - 2, L.n_qb - 1]]))
     _config_case(ress, L, 5, rows=rows, n_tokens=256, label=f"n_kb=4096 q{bq}/k{bk}", max_excluded=0.01)
+
+
+# Layers of one to four blocks: a single token, one partial block, exactly one block,
+# one block plus a token, the 128/64 and 64/128 grids, special tokens, and (budget 2
+# of 3-4 key blocks) small selections that drop a block. Selection against the oracle
+# on every row, sparse and dense attention on every token.
+TINY_LAYERS = [  # (tokens, special tokens, bq, bk, budget or None for the layer's own)
+    (1, 0, 64, 64, None), (37, 0, 64, 64, None), (64, 0, 64, 64, None), (65, 0, 64, 64, None),
+    (37, 0, 128, 128, None), (100, 0, 128, 64, None), (129, 0, 128, 128, None), (200, 0, 64, 128, None),
+    (90, 10, 64, 64, None), (150, 0, 64, 64, 2), (250, 0, 64, 64, 2), (250, 0, 128, 64, 2),
+]
+
+
+@pytest.mark.parametrize("n,spec,bq,bk,budget", TINY_LAYERS)
+def test_layers_of_a_few_blocks(ress, n, spec, bq, bk, budget):
+    import torch
+
+    L = synth.make_layer(1, n, spec, H=2, bq=bq, bk=bk, sparsity=0.5, seed=50 + n + spec, name=f"n{n + spec}")
+    b = None if budget is None else np.full(L.H, budget, np.int32)
+    label = f"N={L.N} {bq}/{bk} budget={b.tolist() if b is not None else L.budgets.tolist()}"
+    say(f"[few blocks] {label} n_qb={L.n_qb} n_kb={L.n_kb}")
+    inputs = device_inputs(L)
+    gpu, dev = gpu_select(L, inputs, rounds=3, budgets=b)
+    ref = oracle_select(L, rounds=3, budgets=b)
+    compare_select(L, gpu, ref, budgets=b, label=label)
+    q, k, v, _ = inputs
+    o = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk,
+                              n_special_tail=L.n_special_tail)
+    od = ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail)
+    torch.cuda.synchronize()
+    hs, ts = _all_tokens(L)
+    compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label=label + " sparse")
+    compare_attn(L, od, hs, ts, label=label + " dense")
