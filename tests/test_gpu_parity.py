@@ -527,14 +527,19 @@ def test_key_block_cap(ress, bq, bk):
     _config_case(ress, L, 5, rows=rows, n_tokens=256, label=f"n_kb=4096 q{bq}/k{bk}", max_excluded=0.01)
 
 
-# Layers of one to four blocks: a single token, one partial block, exactly one block,
+# Layers of one to five blocks: a single token, one partial block, exactly one block,
 # one block plus a token, the 128/64 and 64/128 grids, special tokens, and (budget 2
-# of 3-4 key blocks) small selections that drop a block. Selection against the oracle
+# of 3-4 key blocks) small selections that drop a block; layers of special tokens only
+# (no candidate block: every key block forced, every query block dense), a special
+# tail spanning two key blocks of the 128/64 grid (budget 0: the other rows keep the
+# forced blocks only) and one special token at the end. Selection against the oracle
 # on every row, sparse and dense attention on every token.
-TINY_LAYERS = [  # (tokens, special tokens, bq, bk, budget or None for the layer's own)
+TINY_LAYERS = [  # (patch tokens, special tokens, bq, bk, budget or None for the layer's own)
     (1, 0, 64, 64, None), (37, 0, 64, 64, None), (64, 0, 64, 64, None), (65, 0, 64, 64, None),
     (37, 0, 128, 128, None), (100, 0, 128, 64, None), (129, 0, 128, 128, None), (200, 0, 64, 128, None),
     (90, 10, 64, 64, None), (150, 0, 64, 64, 2), (250, 0, 64, 64, 2), (250, 0, 128, 64, 2),
+    (0, 64, 64, 64, None), (0, 200, 128, 64, None), (180, 20, 128, 64, None), (60, 140, 64, 128, None),
+    (300, 1, 64, 64, None),
 ]
 
 
