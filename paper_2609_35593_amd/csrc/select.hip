@@ -11,7 +11,8 @@
 //  - The contractions are float64 matrix products of the workgroup's rows
 //    (padded to a multiple of 16) with the head's row-major pooled tensors, on
 //    the matrix cores (16x16x4 float64 steps): over channels, the pooled logits
-//    against Kbar and the drift scores and every round's gains against Vbar;
+//    against Kbar and the drift scores (expanded as in Eq. 9; a row's block with
+//    P > 1/2 gets e^T M e directly) and every round's gains against Vbar;
 //    over key blocks, the dense pooled output vbar and the net drift g against
 //    Vbar. The pooled tensor goes from L2 straight into the B operands (each lane
 //    reads 16 contiguous bytes or more of one key block); the A operands are the
