@@ -193,6 +193,25 @@ def criteria_report(ress, L, q, k, v, gram, o_dense, stream):
     return rep
 
 
+def input_stats(ress, L, q, k, v, gram, o_dense, stream):
+    """Sanity statistics of the synthetic layer (not targets): the mean over (head,
+    query block) rows of the pooled map's largest probability max_j P_ij and of its
+    normalised entropy -sum_j P_ij log P_ij / log n_kb (Eq. 1's P, as the selection
+    computes it), and the mean |O| of the dense attention output (small values keep
+    the bf16 output rounding well inside the parity bounds)."""
+    import torch
+
+    sel = ress.ress_select(q, k, v, gram, L.budgets, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail,
+                           want_debug=True, stream=stream)
+    P = sel["prob"].double()
+    ent = -torch.where(P > 0, P * torch.log(P), torch.zeros_like(P)).sum(-1) / math.log(L.n_kb)
+    mean_abs_o = o_dense.float().abs().mean()
+    torch.cuda.synchronize()
+    return {"pooled_row_max_p_mean": round(float(P.max(-1).values.mean()), 4),
+            "pooled_row_entropy_normalised_mean": round(float(ent.mean()), 4),
+            "dense_output_mean_abs": round(float(mean_abs_o), 4)}
+
+
 def masking_report(ress, L, q, k, v, gram, stream):
     """Sec. 3's test of the probability assumption (Fig. 2) on this synthetic layer:
     mask one candidate key block at a time (every query block attends to all other
@@ -535,6 +554,7 @@ def main():
     if args.rounds_sweep:
         sweep = rounds_sweep(ress, L, q, k, v, gram, stream, flush, [int(x) for x in args.rounds_sweep.split(",")])
     ceilings = measured_ceilings(torch, dev)
+    stats = input_stats(ress, L, q, k, v, gram, od, stream)
     criteria = None if args.no_criteria else criteria_report(ress, L, q, k, v, gram, od, stream)
     mask_rep = None if args.no_masking else masking_report(ress, L, q, k, v, gram, stream)
     neigh = None if args.no_neighbours else neighbours_report(ress, L, stream)
@@ -621,6 +641,7 @@ def main():
             "single_block_masking": mask_rep,
             "fused_neighbours": neigh,
             "input_generation_s": round(gen_s, 1),
+            "input_statistics": stats,
         },
     }
     if not args.no_cpu_baseline:
