@@ -78,3 +78,50 @@ def test_random_small_layer(ress, idx):
     hs, ts = hs.ravel().astype(np.int32), ts.ravel().astype(np.int32)
     compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label=label + " sparse")
     compare_attn(L, od, hs, ts, label=label + " dense")
+
+
+# Medium layers (4-12 views of 500-1400 patch tokens): larger budgets, so the
+# restoration rounds swap many blocks at once; every selection row, attention on a
+# stratified sample of tokens.
+N_MEDIUM = 12
+
+
+def draw_medium(n=N_MEDIUM, seed=35593):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        H = int(rng.integers(2, 5))
+        cases.append(dict(views=int(rng.integers(4, 13)), patch=int(rng.integers(500, 1401)),
+                          special=int(rng.choice([0, 1, 5])), H=H,
+                          bq=int(rng.choice([64, 128])), bk=int(rng.choice([64, 128])),
+                          sparsity=[round(float(x), 3) for x in rng.uniform(0.5, 0.95, size=H)],
+                          rounds=int(rng.choice([1, 3, 5, 8])), criterion=int(rng.choice([0, 0, 1, 2])),
+                          seed=int(rng.integers(0, 1 << 30))))
+    return cases
+
+
+MEDIUM = draw_medium()
+
+
+@pytest.mark.parametrize("idx", range(N_MEDIUM))
+def test_random_medium_layer(ress, idx):
+    import torch
+
+    from gpu_helpers import sample_tokens
+
+    c = MEDIUM[idx]
+    L = synth.make_layer(c["views"], c["patch"], c["special"], H=c["H"], bq=c["bq"], bk=c["bk"],
+                         sparsity=np.asarray(c["sparsity"]), seed=c["seed"], name=f"medium{idx}")
+    label = (f"medium {idx}: N={L.N} H={L.H} {L.bq}/{L.bk} special={L.n_special_tail} "
+             f"budgets={L.budgets.tolist()} R={c['rounds']} criterion={c['criterion']}")
+    say(f"[random layer] {label}")
+    inputs = device_inputs(L)
+    gpu, dev = gpu_select(L, inputs, rounds=c["rounds"], criterion=c["criterion"])
+    ref = oracle_select(L, rounds=c["rounds"], criterion=c["criterion"])
+    compare_select(L, gpu, ref, label=label, criterion=c["criterion"])
+    q, k, v, _ = inputs
+    o = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk,
+                              n_special_tail=L.n_special_tail)
+    torch.cuda.synchronize()
+    hs, ts = sample_tokens(L, 512, seed=idx)
+    compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label=label + " sparse")
