@@ -1,7 +1,9 @@
 """ress_select_noalloc, the selection entry point for callers that cannot
 allocate (its workspace is the library's fixed per-GPU scratch array), against
 ress_select with a caller workspace on the same inputs: every output identical,
-on two calls in a row, the second on a smaller layer. Also the host-side checks
+on calls in a row over layers that shrink (32 views, 8 views, a 301-token layer on
+the 64-token grid) and then grow again (32 views on the 128/64 grid), so that
+nothing left in the scratch array from a previous call can matter. Also the host-side checks
 (no GPU work): a shape whose workspace exceeds the scratch array, and a pooled
 state the caller cannot have written there."""
 import ctypes as C
@@ -35,11 +37,14 @@ def _outputs(L, dev):
                 prob_out=torch.full((L.H, L.n_qb, L.n_kb), -7.0, dtype=torch.float64, device=dev))
 
 
-def test_noalloc_matches_select_twice(ress):
+def test_noalloc_matches_select_in_a_row(ress):
     import torch
 
     dev = "cuda:0"
-    for L in (synth.make_config("32v"), synth.make_config("8v", sparsity=0.5)):
+    layers = (synth.make_config("32v"), synth.make_config("8v", sparsity=0.5),
+              synth.make_layer(1, 300, 1, H=3, block=64, sparsity=0.5, seed=77, name="n301"),
+              synth.make_config("32v", bk=64))
+    for L in layers:
         say(f"[noalloc] {L.name} H={L.H} N={L.N} n_kb={L.n_kb}")
         q, k, v, gram = device_inputs(L, dev)
         kw = dict(bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail, rounds=5)
