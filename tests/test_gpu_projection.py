@@ -66,7 +66,10 @@ def _qkv_bounds(x, w_qkv, H):
 
 
 CASES = [(4, 1000, 128, 128, 11), (4, 777, 64, 128, 12), (16, 2755, 128, 64, 13), (4, 1, 64, 64, 15),
-         (8, 130, 128, 64, 16)]
+         (8, 130, 128, 64, 16),
+         # 768-wide model (3 output tiles per projection), token counts at and
+         # around the 256-row tile edge
+         (12, 255, 64, 64, 17), (12, 256, 128, 128, 18), (12, 257, 128, 64, 19), (8, 513, 64, 128, 20)]
 
 
 @pytest.mark.parametrize("H,N,bq,bk,seed", CASES)
@@ -124,7 +127,7 @@ def test_qkv_projection_32v_sampled(ress):
         assert torch.equal(fused[name], plain[name]), name
 
 
-@pytest.mark.parametrize("H,N,seed", [(4, 1000, 21), (16, 2755, 22)])
+@pytest.mark.parametrize("H,N,seed", [(4, 1000, 21), (16, 2755, 22), (12, 257, 23), (8, 7, 24), (4, 256, 25)])
 def test_out_projection_residual(ress, H, N, seed):
     import torch
 

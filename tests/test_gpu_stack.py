@@ -41,7 +41,7 @@ def _f64(bits):
     return synth.bf16_bits_to_f32(bits).astype(np.float64)
 
 
-@pytest.mark.parametrize("H,N,seed", [(4, 1000, 41), (16, 2755, 42)])
+@pytest.mark.parametrize("H,N,seed", [(4, 1000, 41), (16, 2755, 42), (12, 257, 43), (8, 7, 44)])
 def test_out_projection_residual_f32(ress, H, N, seed):
     import torch
 
