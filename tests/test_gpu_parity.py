@@ -563,3 +563,28 @@ def test_layers_of_a_few_blocks(ress, n, spec, bq, bk, budget):
     hs, ts = _all_tokens(L)
     compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label=label + " sparse")
     compare_attn(L, od, hs, ts, label=label + " dense")
+
+
+@pytest.mark.parametrize("H", [255, 256])
+def test_many_heads(ress, H):
+    """The head limit (256) and an odd head count on a small layer: per-head budgets
+    from per-head sparsities, every selection row against the oracle, sparse and
+    dense attention on every token."""
+    import torch
+
+    rng = np.random.default_rng(H)
+    L = synth.make_layer(1, 300, 5, H=H, block=64, sparsity=rng.uniform(0.2, 0.8, size=H), seed=H, name=f"h{H}")
+    label = f"H={H} N={L.N} budgets {L.budgets.min()}..{L.budgets.max()}"
+    say(f"[many heads] {label}")
+    inputs = device_inputs(L)
+    gpu, dev = gpu_select(L, inputs, rounds=3)
+    ref = oracle_select(L, rounds=3)
+    compare_select(L, gpu, ref, label=label)
+    q, k, v, _ = inputs
+    o = ress.ress_sparse_attn(q, k, v, dev["kept_count"], dev["kept_idx"], bq=L.bq, bk=L.bk,
+                              n_special_tail=L.n_special_tail)
+    od = ress.ress_dense_attn(q, k, v, bq=L.bq, bk=L.bk, n_special_tail=L.n_special_tail)
+    torch.cuda.synchronize()
+    hs, ts = _all_tokens(L)
+    compare_attn(L, o, hs, ts, kept_count=gpu["kept_count"], kept_idx=gpu["kept_idx"], label=label + " sparse")
+    compare_attn(L, od, hs, ts, label=label + " dense")
