@@ -9,29 +9,37 @@
 // the lane except for one exchange with lane l^32, and the probabilities already
 // sit in the B-operand layout of O^T = V^T P^T.
 //
-// Keys are consumed in 128-key tiles (one 128-key block, or two 64-key blocks
-// of the list) split into 64-key halves, software-pipelined over halves: the
-// step that forms the probabilities of half n also issues the score MFMAs of
-// half n+1 and the PV MFMAs of half n-1, so one basic block holds 16 MFMAs next
-// to the softmax arithmetic and the matrix and vector pipes run side by side.
-// K and V tiles move from global memory straight into LDS (global_load_lds, 16
-// bytes per lane, 1 KB per wave instruction) in two-slot rings; one barrier per
-// tile, between its two halves, both publishes the tiles loaded one tile earlier
-// and frees the slots the next loads overwrite (K of tile t+2, V of tile t+1).
-// Tiles stay row-major (64 channels = 128 bytes per key) with their 16-byte
-// chunks XOR-swizzled per key; the swizzle is applied by choosing each lane's
-// source chunk, since a DMA instruction fills LDS contiguously. The V^T operand
-// comes from ds_read_b64_tr_b16: within 16 lanes, lane s points at 4 channels
-// of key k0 + s/4 and lane i receives channel d0 + i of keys k0..k0+3, which is
-// the transpose the PV product needs.
+// Keys are consumed in 64-key chunks (one 64-key block of the kept list, or half
+// of a 128-key block). A chunk is two 32-key sub-tiles; for each, a wave issues
+// its 4 score MFMAs, forms the probabilities and issues its 4 PV MFMAs, in that
+// order. Latency is hidden by occupancy rather than by pipelining inside a wave:
+// K and V chunks sit in two-slot rings of 8 KB per tensor and slot (32 KB per
+// workgroup), and the kernel fits 128 registers, so four 128-query workgroups
+// share a CU (four waves per SIMD), and the matrix and vector pipes of a SIMD
+// serve whichever of its waves is ready. (Measured: at D = 64 the softmax needs
+// about as many issue slots as the MFMAs; two waves per SIMD with a software
+// pipeline reached the same rate as three without one, four waves run 4-8%
+// faster.)
+//
+// Chunks move from global memory straight into LDS (buffer_load ... lds, 16
+// bytes per lane, 1 KB per wave instruction, 32-bit offsets against a per-head
+// buffer resource): chunk c+1 is loaded while chunk c is computed, and one
+// barrier per chunk both publishes chunk c+1 and frees chunk c's slots. Rows stay
+// row-major (64 channels = 128 bytes per key) with their 16-byte chunks
+// XOR-swizzled per key; the swizzle is applied by choosing each lane's source
+// chunk, since a DMA instruction fills LDS contiguously. The V^T operand comes
+// from ds_read_b64_tr_b16: within 16 lanes, lane s points at 4 channels of key
+// k0 + s/4 and lane i receives channel d0 + i of keys k0..k0+3, which is the
+// transpose the PV product needs. The kept list is read through the scalar
+// cache (wave-uniform addresses).
 //
 // Softmax: base-2 exponentials; row sums over the bf16-rounded probabilities
 // (the values the PV product consumes) with packed bf16 dot products. There is
-// no per-half maximum: every row starts with reference 0 and forms its
-// probabilities against its reference; only when a half's sum exceeds 2^50, or
-// the row's running sum is still below 2^-100, is the half redone against its
-// true maximum (a result within +-40 of 0 is rounded to 0) and O rescaled.
-// While every row of a wave has reference 0, the wave runs a copy of the tile
+// no per-tile maximum: every row starts with reference 0 and forms its
+// probabilities against its reference; only when a sub-tile's sum exceeds 2^50,
+// or the row's running sum is still below 2^-100, is the sub-tile redone against
+// its true maximum (a result within +-40 of 0 is rounded to 0) and O rescaled.
+// While every row of a wave has reference 0, the wave runs a copy of the chunk
 // loop whose probabilities are exp2 of the score accumulators with nothing
 // else: Q is multiplied by scale*log2(e) when its fragments are loaded (one extra
 // bf16 rounding of Q), so the accumulators are base-2 logits. A wave whose first
@@ -40,7 +48,7 @@
 // Softmax is invariant to the reference, so this changes rounding only.
 //
 // Workgroups are numbered so that neighbouring query blocks of a head share an
-// XCD and its L2, where their K/V tiles are re-read, and heads of different cost
+// XCD and its L2, where their K/V chunks are re-read, and heads of different cost
 // (ragged budgets) still split evenly over the XCDs (see row_of).
 #include <type_traits>
 
@@ -56,10 +64,10 @@ typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr float kSumLimit = 0x1p50f;  // largest probability sum a half may reach
+constexpr float kSumLimit = 0x1p50f;  // largest probability sum a sub-tile may reach
 constexpr float kTiny = 0x1p-100f;    // a row whose running sum is below this has no usable reference
 constexpr float kZeroBand = 40.f;     // references within +-40 (base-2 logits) become 0
-constexpr float kStartBand = 24.f;    // first-half maxima a wave may have to start with reference 0
+constexpr float kStartBand = 24.f;    // first-chunk maxima a wave may have to start with reference 0
 
 __device__ __forceinline__ unsigned int bf16_bits(float x)
 {
@@ -135,22 +143,21 @@ __device__ __forceinline__ bool row_of(const AttnParams &p, bool sparse, int xcd
     return true;
 }
 
-// Two waves per SIMD for 128-query blocks (two 64 KB workgroups per CU); the LDS
-// allows 64-query blocks only one.
+// Four waves per SIMD for 128-query blocks (four 32 KB workgroups per CU); 64-query
+// blocks are held to two by the LDS (five 2-wave workgroups per CU).
 template <int BQ, int BK, bool SPARSE>
-__global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 2 : 1) attn_kernel(const AttnParams p)
+__global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 4 : 2) attn_kernel(const AttnParams p)
 {
     constexpr int T = BQ * 2;                 // threads
     constexpr int NW = BQ / 32;               // waves
-    constexpr int EPT = BK == 128 ? 1 : 2;    // kept-list entries per 128-key tile
-    constexpr int LPH = 64 * 8 / T;           // 16-byte DMA loads per thread, tensor and half
-    constexpr int TILE = 128 * 128;           // bytes of one K (or V) tile
-    constexpr int HALF = TILE / 2;
-    static_assert(64 * 8 % T == 0 && LPH >= 1, "a half tile must split evenly over the threads");
-    __shared__ __attribute__((aligned(1024))) unsigned char k_lds0[TILE];
-    __shared__ __attribute__((aligned(1024))) unsigned char k_lds1[TILE];
-    __shared__ __attribute__((aligned(1024))) unsigned char v_lds0[TILE];
-    __shared__ __attribute__((aligned(1024))) unsigned char v_lds1[TILE];
+    constexpr int CPE = BK / 64;              // 64-key chunks per kept-list entry
+    constexpr int LPC = 64 * 8 / T;           // 16-byte DMA loads per thread, tensor and chunk
+    constexpr int SLOT = 64 * 128;            // bytes of one chunk of K (or V)
+    static_assert(64 * 8 % T == 0 && LPC >= 1, "a chunk must split evenly over the threads");
+    __shared__ __attribute__((aligned(1024))) unsigned char k_s0[SLOT];
+    __shared__ __attribute__((aligned(1024))) unsigned char k_s1[SLOT];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_s0[SLOT];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_s1[SLOT];
 
     const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
     int h, i;
@@ -194,80 +201,48 @@ __global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 2 : 1) attn_kernel(const A
     } else {
         n_ent = n_kb;
     }
-    const int L = (n_ent + EPT - 1) / EPT;  // 128-key tiles
+    const int C = n_ent * CPE;  // 64-key chunks
 
-    // Kept block indices, read 64 at a time: lane l of idx_lo holds entry 64c + l of
-    // the list, idx_hi the next 64, loaded one chunk ahead of use.
-    int idx_lo = -1, idx_hi = -1;
-    auto load_chunk = [&](int c) __attribute__((always_inline)) -> int {
-        const int t = 64 * c + lane;
-        return t < n_ent ? list[t] : -1;
-    };
-    if constexpr (SPARSE) {
-        idx_lo = load_chunk(0);
-        idx_hi = load_chunk(1);
-    }
-    // Block index of entry e (-1 past the end); called for e = 0, 1, 2, ... in order.
-    auto entry = [&](int e) __attribute__((always_inline)) -> int {
-        if constexpr (SPARSE) {
-            if (e > 0 && (e & 63) == 0) {
-                idx_lo = idx_hi;
-                idx_hi = load_chunk((e >> 6) + 1);
-            }
-            return __builtin_amdgcn_readlane(idx_lo, e & 63);
-        } else {
-            return e < n_ent ? e : -1;
-        }
-    };
-    auto fetch_tile = [&](int t, int (&jt)[EPT]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) jt[e] = entry(t * EPT + e);
+    // Kept block indices through the scalar cache (wave-uniform addresses; the list
+    // is read-only here).
+    typedef const __attribute__((address_space(4))) int32_t cint32;
+    const cint32 *klist = (const cint32 *)list;
+    auto block_of = [&](int ch) __attribute__((always_inline)) -> int {
+        const int e = ch / CPE;
+        if constexpr (SPARSE) return e < n_ent ? klist[e] : -1;
+        else return e < n_ent ? e : -1;
     };
     auto valid = [&](int j) __attribute__((always_inline)) { return j >= 0 && j < n_kb; };
-    // First token of half hf of a tile, and how many of its 64 keys are real.
-    auto half_row0 = [&](const int (&jt)[EPT], int hf) __attribute__((always_inline)) -> int {
-        if constexpr (EPT == 1) return valid(jt[0]) ? jt[0] * 128 + 64 * hf : 0;
-        else return valid(jt[hf]) ? jt[hf] * 64 : 0;
+    // First token of chunk ch of block j, and how many of its 64 keys are real.
+    auto chunk_row0 = [&](int j, int ch) __attribute__((always_inline)) -> int {
+        return valid(j) ? j * BK + 64 * (ch & (CPE - 1)) : 0;
     };
-    auto half_keys = [&](const int (&jt)[EPT], int hf) __attribute__((always_inline)) -> int {
-        if constexpr (EPT == 1) return valid(jt[0]) ? max(0, min(64, N - jt[0] * 128 - 64 * hf)) : 0;
-        else return valid(jt[hf]) ? min(64, N - jt[hf] * 64) : 0;
+    auto chunk_keys = [&](int j, int ch) __attribute__((always_inline)) -> int {
+        return valid(j) ? max(0, min(64, N - j * BK - 64 * (ch & (CPE - 1)))) : 0;
     };
 
-    // DMA: thread-constant byte offsets within a 64-row half (row r of the half,
-    // the logical chunk that belongs at physical chunk lane&7).
-    const unsigned char *kbytes = reinterpret_cast<const unsigned char *>(p.k + head * kD);
-    const unsigned char *vbytes = reinterpret_cast<const unsigned char *>(p.v + head * kD);
-    unsigned int doff[LPH];
+    // This head's K and V as buffer resources (byte offsets below N * 128 < 2^31).
+    const __amdgpu_buffer_rsrc_t krs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k + head * kD), 0, N * 128, 0x00020000);
+    const __amdgpu_buffer_rsrc_t vrs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v + head * kD), 0, N * 128, 0x00020000);
+    // DMA lane constants: load u of a thread fills row r0 + 8 NW u of the slot, at
+    // physical chunk lane & 7, from source chunk (lane & 7) ^ swz(row) (the same for
+    // every u: the swizzle depends on row bits 1-3 only).
+    const int r0 = wave * 8 + (lane >> 3);
+    const unsigned int coff = (unsigned int)(((lane & 7) ^ swz(r0)) << 4);
+    // Rows row0..row0+63 of one tensor into a slot; rows past N repeat row N-1.
+    auto dma_chunk = [&](__amdgpu_buffer_rsrc_t rs, int row0, unsigned char *dst) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < LPH; ++u) {
-        const int r = (u * NW + wave) * 8 + (lane >> 3);
-        doff[u] = (unsigned int)(r * 128 + (((lane & 7) ^ swz(r)) << 4));
-    }
-    // Rows row0..row0+63 of one tensor into a half slot; rows past N repeat row N-1.
-    auto dma_half = [&](const unsigned char *src, int row0, unsigned char *dst) __attribute__((always_inline)) {
-        if (row0 + 64 <= N) {
-            const unsigned char *s = src + (size_t)row0 * 128;
-#pragma unroll
-            for (int u = 0; u < LPH; ++u)
-                __builtin_amdgcn_global_load_lds((const void *)(s + doff[u]), (lds_void *)(dst + (u * NW + wave) * 1024), 16, 0, 0);
-        } else {
-#pragma unroll
-            for (int u = 0; u < LPH; ++u) {
-                const int r = (u * NW + wave) * 8 + (lane >> 3);
-                const int row = min(row0 + r, N - 1);
-                __builtin_amdgcn_global_load_lds((const void *)(src + (size_t)row * 128 + (doff[u] & 127)),
-                                                 (lds_void *)(dst + (u * NW + wave) * 1024), 16, 0, 0);
-            }
+        for (int u = 0; u < LPC; ++u) {
+            const int row = min(row0 + r0 + 8 * NW * u, N - 1);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(dst + (u * NW + wave) * 1024), 16,
+                                                     (unsigned int)(row * 128) + coff, 0, 0, 0);
         }
     };
-    auto dma_tile = [&](const unsigned char *src, const int (&jt)[EPT], unsigned char *dst) __attribute__((always_inline)) {
-        dma_half(src, half_row0(jt, 0), dst);
-        dma_half(src, half_row0(jt, 1), dst + HALF);
-    };
 
-    // Per-lane LDS byte offsets of the operand reads (tile-relative; the key
-    // offset of a half / sub-tile is added as an immediate).
+    // Per-lane LDS byte offsets of the operand reads (chunk-relative; the key offset
+    // of a sub-tile is added as an immediate).
     int koff[4];  // score operand: key ql, logical chunk 2kk+hh
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) koff[kk] = ql * 128 + (((2 * kk + hh) ^ swz(ql)) << 4);
@@ -292,105 +267,89 @@ __global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 2 : 1) attn_kernel(const A
         for (int v = 0; v < 16; ++v) acc_o[dh][v] = 0.f;
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-    // S^T of one half: two 32-key sub-tiles, 4 MFMAs each.
-    auto qk = [&](const unsigned char *kt, int hf, f32x16 (&s)[2]) __attribute__((always_inline)) {
+    // S^T of sub-tile t (32 keys) of a chunk: 4 MFMAs.
+    auto qk = [&](const unsigned char *kt, int t, f32x16 &s) __attribute__((always_inline)) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
+        for (int v = 0; v < 16; ++v) s[v] = 0.f;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) s[t][v] = 0.f;
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + hf * HALF + t * 32 * 128 + koff[kk]);
-                s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[t], 0, 0, 0);
-            }
+        for (int kk = 0; kk < 4; ++kk) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kt + t * 32 * 128 + koff[kk]);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s, 0, 0, 0);
         }
     };
-    // O^T += V^T P^T for one half, 16 keys per MFMA.
-    auto pv = [&](const unsigned char *vt, int hf, const bf16x8 (&pb)[2][2]) __attribute__((always_inline)) {
+    // O^T += V^T P^T for sub-tile t, 16 keys per MFMA.
+    auto pv = [&](const unsigned char *vt, int t, const bf16x8 (&pb)[2]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-            for (int u = 0; u < 2; ++u)
-#pragma unroll
-                for (int dh = 0; dh < 2; ++dh) {
-                    const unsigned char *base = vt + hf * HALF + (t * 32 + u * 16) * 128;
-                    const s16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(base + voff[dh][0]));
-                    const s16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(base + voff[dh][1]));
-                    const bf16x8 a = __builtin_bit_cast(
-                        bf16x8, (short __attribute__((__vector_size__(8 * sizeof(short))))){
-                                    r0[0], r0[1], r0[2], r0[3], r1[0], r1[1], r1[2], r1[3]});
-                    acc_o[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t][u], acc_o[dh], 0, 0, 0);
-                }
-    };
-    // Key of element (t, v) of a half: t 32 + (v / 4) 8 + (v % 4) + 4 hh; compared as
-    // 4 hh >= nv - (the lane-independent part), a scalar per element.
-    const int hh4 = hh * 4;
-    auto mask = [&](f32x16 (&s)[2], int nv) __attribute__((always_inline)) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int lim = __builtin_amdgcn_readfirstlane(nv - (t * 32 + (v >> 2) * 8 + (v & 3)));
-                if (hh4 >= lim) s[t][v] = -INFINITY;
+            for (int dh = 0; dh < 2; ++dh) {
+                const unsigned char *base = vt + (t * 32 + u * 16) * 128;
+                const s16x4 r0v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(base + voff[dh][0]));
+                const s16x4 r1v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(base + voff[dh][1]));
+                const bf16x8 a = __builtin_bit_cast(
+                    bf16x8, (short __attribute__((__vector_size__(8 * sizeof(short))))){
+                                r0v[0], r0v[1], r0v[2], r0v[3], r1v[0], r1v[1], r1v[2], r1v[3]});
+                acc_o[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[u], acc_o[dh], 0, 0, 0);
             }
     };
-    // Probabilities of sub-tile t (32 keys) of a half, exp2(s) when every row has
-    // reference 0 (Z), else exp2(s * cw - mref); adds the bf16-rounded values to
-    // the lane's partial sums.
-    auto probs_part = [&](auto z, const f32x16 (&s)[2], bf16x8 (&pb)[2][2], int t, float &l0,
-                          float &l1) __attribute__((always_inline)) {
+    // Key of element v of sub-tile t: t 32 + (v / 4) 8 + (v % 4) + 4 hh; compared as
+    // 4 hh >= nv - (the lane-independent part), a scalar per element.
+    const int hh4 = hh * 4;
+    auto mask = [&](f32x16 &s, int nv, int t) __attribute__((always_inline)) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int lim = __builtin_amdgcn_readfirstlane(nv - (t * 32 + (v >> 2) * 8 + (v & 3)));
+            if (hh4 >= lim) s[v] = -INFINITY;
+        }
+    };
+    // Probabilities of a sub-tile, exp2(s) when every row has reference 0 (z), else
+    // exp2(s * cw - mref); returns the lane's sum of the bf16-rounded values.
+    auto probs = [&](auto z, const f32x16 &s, bf16x8 (&pb)[2]) __attribute__((always_inline)) -> float {
+        float l0 = 0.f, l1 = 0.f;
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             float e[8];
 #pragma unroll
             for (int jj = 0; jj < 8; ++jj) {
-                const float x = s[t][u * 8 + jj];
+                const float x = s[u * 8 + jj];
                 e[jj] = __builtin_amdgcn_exp2f(decltype(z)::value ? x : fmaf(x, cw, -mref));
             }
-            pb[t][u] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
-                              (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
+            pb[u] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
+                           (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
 #pragma unroll
             for (int jj = 0; jj < 8; jj += 4) {
-                l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][u][jj], pb[t][u][jj + 1]}, ones, l0, false);
-                l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][u][jj + 2], pb[t][u][jj + 3]}, ones, l1, false);
+                l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[u][jj], pb[u][jj + 1]}, ones, l0, false);
+                l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[u][jj + 2], pb[u][jj + 3]}, ones, l1, false);
             }
         }
-    };
-    // Tile-loop variants: every row's reference is 0 (zero), or per-row references (general).
-    using general = std::integral_constant<bool, false>;
-    using zero = std::integral_constant<bool, true>;
-    // All probabilities of one half against the current references; returns the lane's sum.
-    auto probs = [&](const f32x16 (&s)[2], bf16x8 (&pb)[2][2]) __attribute__((always_inline)) -> float {
-        float l0 = 0.f, l1 = 0.f;
-        probs_part(general{}, s, pb, 0, l0, l1);
-        probs_part(general{}, s, pb, 1, l0, l1);
         return l0 + l1;
     };
-    // Accept the half's probabilities, or redo them against a new reference
-    // (rescaling O and the running sum) when the half's sum exceeds kSumLimit,
+    // Chunk-loop variants: every row's reference is 0 (zero), or per-row references (general).
+    using general = std::integral_constant<bool, false>;
+    using zero = std::integral_constant<bool, true>;
+    // Accept the sub-tile's probabilities, or redo them against a new reference
+    // (rescaling O and the running sum) when the sub-tile's sum exceeds kSumLimit,
     // the row still has no mass above kTiny, or (zero variant) a row of the wave
-    // already left reference 0 earlier in this tile.
-    auto settle = [&](auto z, const f32x16 (&s)[2], bf16x8 (&pb)[2][2], float lh) __attribute__((always_inline)) {
+    // already left reference 0 in this chunk.
+    auto settle = [&](auto z, const f32x16 &s, bf16x8 (&pb)[2], float lh) __attribute__((always_inline)) {
         constexpr bool Z = decltype(z)::value;
         if (__any(!(lh <= kSumLimit) || lrow + lh < kTiny || (Z && mref != 0.f))) {
             float tmax = -INFINITY;
 #pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) tmax = fmaxf(tmax, s[t][v]);
+            for (int v = 0; v < 16; ++v) tmax = fmaxf(tmax, s[v]);
             tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * cw;
             // Decisions about the row's mass use the row's running sum: lanes l and
             // l^32 each sum half of the row's keys (one of them may have no mass yet
             // while the row has), and both must take the same reference.
             const float lsum = lrow + __shfl_xor(lrow, 32);
             // The reference only rises, except while the row has no usable mass yet:
-            // then it may fall to this half's maximum, but not below
+            // then it may fall to this sub-tile's maximum, but not below
             // mref + log2(lsum), an upper bound of every earlier logit of the row, so
             // that the rescaled running sums stay at most 1 (finite).
             float mnew = fmaxf(mref, tmax);
             // (log2 of a denormal sum may come back as -inf: -149 bounds it.)
             if (lsum < kTiny) mnew = lsum > 0.f ? fmaxf(tmax, mref + fmaxf(__log2f(lsum), -149.f)) : tmax;
-            if (tmax == -INFINITY) mnew = mref;  // a fully masked half says nothing
+            if (tmax == -INFINITY) mnew = mref;  // a fully masked sub-tile says nothing
             if (fabsf(mnew) <= kZeroBand) mnew = 0.f;
             // A row without mass has nothing to rescale (and 0 * exp2(large) must not
             // happen); otherwise the factor is applied as two halves, each finite
@@ -403,105 +362,83 @@ __global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 2 : 1) attn_kernel(const A
                 for (int v = 0; v < 16; ++v) acc_o[dh][v] = (acc_o[dh][v] * alpha) * alpha;
             mref = mnew;
             if (Z) zref = __all(mref == 0.f);
-            lh = probs(s, pb);
+            lh = probs(general{}, s, pb);
         }
         lrow += lh;
     };
-    // One pipeline step: softmax of the current half (scores sc, nv real keys)
-    // beside the score MFMAs of the next half (kt, khf -> sn) and the PV MFMAs
-    // of the previous half (probabilities pp, vt, vhf).
-    auto step = [&](auto z, f32x16 (&sc)[2], bf16x8 (&pc)[2][2], int nv, f32x16 (&sn)[2], const unsigned char *kt,
-                    int khf, const bf16x8 (&pp)[2][2], const unsigned char *vt, int vhf) __attribute__((always_inline)) {
-        if (nv < 64) {
-            // A real branch: only partial halves pay for the mask (the empty asm
-            // keeps the compiler from if-converting it into every step).
-            asm volatile("" ::: "memory");
-            mask(sc, nv);
+
+    int nv0 = 0, nv1 = 0;  // real keys of chunks ch and ch+1
+    // Chunk ch from slots (ks, vs); first the DMA of chunk ch+1 into (kd, vd), the
+    // slots of chunk ch-1 (free since the barrier that ended it).
+    auto iter = [&](auto z, int ch, const unsigned char *ks, const unsigned char *vs, unsigned char *kd,
+                    unsigned char *vd) __attribute__((always_inline)) {
+        if (ch + 1 < C) {
+            const int j1 = block_of(ch + 1);
+            nv1 = __builtin_amdgcn_readfirstlane(chunk_keys(j1, ch + 1));
+            const int row1 = chunk_row0(j1, ch + 1);
+            dma_chunk(krs, row1, kd);
+            dma_chunk(vrs, row1, vd);
         }
-        // Two scheduling regions. First the score MFMAs of the next half (their
-        // results are consumed at the next step) beside the softmax of sub-tile 0,
-        // then the PV MFMAs of the previous half beside the softmax of sub-tile 1.
-        // In each, the compiler's MFMA/LDS interleaving strategy 0 (measured: the
-        // same results, dense 1.5% and the 128/64 grid 1% faster).
-        float l0 = 0.f, l1 = 0.f;
-        __builtin_amdgcn_iglp_opt(0);
-        qk(kt, khf, sn);
-        probs_part(z, sc, pc, 0, l0, l1);
-        __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_iglp_opt(0);
-        pv(vt, vhf, pp);
-        probs_part(z, sc, pc, 1, l0, l1);
-        const float lh = l0 + l1;
-        settle(z, sc, pc, lh);
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            f32x16 s;
+            bf16x8 pb[2];
+            qk(ks, t, s);
+            if (nv0 < 64) {
+                // A real branch: only partial chunks pay for the mask (the empty asm
+                // keeps the compiler from if-converting it into every sub-tile).
+                asm volatile("" ::: "memory");
+                mask(s, nv0, t);
+            }
+            const float lh = probs(z, s, pb);
+            settle(z, s, pb, lh);
+            pv(vs, t, pb);
+        }
+        wait_vm_all();    // this wave's loads of chunk ch+1 have landed
+        __syncthreads();  // ... and every wave's; chunk ch's slots are no longer read
+        nv0 = nv1;
     };
 
-    f32x16 sA[2], sB[2];
-    bf16x8 pA[2][2], pB[2][2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int u = 0; u < 2; ++u) pB[t][u] = bf16x8{};
-    int jt0[EPT], jt1[EPT], jt2[EPT];
-
-    // Tile it (it = 0 .. L-1): K in kc, V in vc; K of tile it+1 in kn; V of tile
-    // it-1 in vp. sA holds the scores of (it, half 0), pB the probabilities of
-    // (it-1, half 1).
-    auto iter = [&](auto z, int it, unsigned char *kc, const unsigned char *kn, const unsigned char *vc,
-                    unsigned char *vp) __attribute__((always_inline)) {
-        fetch_tile(it + 2, jt2);
-        step(z, sA, pA, half_keys(jt0, 0), sB, kc, 1, pB, vp, 1);
-        wait_vm_all();    // this wave's loads of K(it+1) and V(it) have landed
-        __syncthreads();  // ... and every wave's; K(it) and V(it-1) are no longer read
-        if (it + 2 < L) dma_tile(kbytes, jt2, kc);
-        if (it + 1 < L) dma_tile(vbytes, jt1, vp);
-        step(z, sB, pB, half_keys(jt0, 1), sA, kn, 0, pA, vc, 0);
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-            jt0[e] = jt1[e];
-            jt1[e] = jt2[e];
+    if (C > 0) {
+        {
+            const int j0 = block_of(0);
+            nv0 = __builtin_amdgcn_readfirstlane(chunk_keys(j0, 0));
+            const int row0 = chunk_row0(j0, 0);
+            dma_chunk(krs, row0, k_s0);
+            dma_chunk(vrs, row0, v_s0);
         }
-    };
-
-    if (L > 0) {
-        fetch_tile(0, jt0);
-        fetch_tile(1, jt1);
-        // The first step multiplies zero probabilities with V slot 1, half 1.
-        for (int u = tid; u < HALF / 16; u += T) reinterpret_cast<uint4 *>(v_lds1 + HALF)[u] = make_uint4(0, 0, 0, 0);
-        dma_tile(kbytes, jt0, k_lds0);
-        if (L > 1) dma_tile(kbytes, jt1, k_lds1);
-        dma_tile(vbytes, jt0, v_lds0);
         wait_vm_all();
         __syncthreads();
-        qk(k_lds0, 0, sA);
         {
-            // Start with reference 0 only if every row's first logits lie within
+            // Start with reference 0 only if every row's first 64 logits lie within
             // kStartBand; otherwise use unscaled Q (exact scores) from the start.
             float m0 = -INFINITY;
 #pragma unroll
-            for (int t = 0; t < 2; ++t)
+            for (int t = 0; t < 2; ++t) {
+                f32x16 s0;
+                qk(k_s0, t, s0);
 #pragma unroll
-                for (int v = 0; v < 16; ++v) m0 = fmaxf(m0, sA[t][v]);
+                for (int v = 0; v < 16; ++v) m0 = fmaxf(m0, s0[v]);
+            }
             m0 = fmaxf(m0, __shfl_xor(m0, 32));
             zref = __all(fabsf(m0) <= kStartBand);
             if (!zref) {
                 load_q(false);
                 cw = c;
-                qk(k_lds0, 0, sA);
+                wait_vm_all();  // Q lands here, not at the first MFMA of every chunk
             }
         }
-        int it = 0;
+        int ch = 0;
         // A wave leaves the zero variant (for good) when a row's reference leaves 0;
         // its Q stays pre-scaled (cw = 1), so every score of a row has one form.
         for (;;) {
-            if (zref) iter(zero{}, it, k_lds0, k_lds1, v_lds0, v_lds1);
-            else iter(general{}, it, k_lds0, k_lds1, v_lds0, v_lds1);
-            if (++it >= L) break;
-            if (zref) iter(zero{}, it, k_lds1, k_lds0, v_lds1, v_lds0);
-            else iter(general{}, it, k_lds1, k_lds0, v_lds1, v_lds0);
-            if (++it >= L) break;
+            if (zref) iter(zero{}, ch, k_s0, v_s0, k_s1, v_s1);
+            else iter(general{}, ch, k_s0, v_s0, k_s1, v_s1);
+            if (++ch >= C) break;
+            if (zref) iter(zero{}, ch, k_s1, v_s1, k_s0, v_s0);
+            else iter(general{}, ch, k_s1, v_s1, k_s0, v_s0);
+            if (++ch >= C) break;
         }
-        // PV of the last half; its tile sits in V slot (L-1) % 2.
-        pv((L & 1) ? v_lds0 : v_lds1, 1, pB);
     }
 
     // Each lane summed half of its row's keys; lanes l and l^32 share the row.
