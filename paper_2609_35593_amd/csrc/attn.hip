@@ -201,7 +201,14 @@ __global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 4 : 2) attn_kernel(const A
     } else {
         n_ent = n_kb;
     }
-    const int C = n_ent * CPE;  // 64-key chunks
+    int C = n_ent * CPE;  // 64-key chunks
+    if (CPE == 2 && n_ent > 0 && N - (n_kb - 1) * BK <= 64) {
+        // The last block holds at most 64 tokens: its second chunk is empty.
+        int jl;
+        if constexpr (SPARSE) jl = list[n_ent - 1];
+        else jl = n_ent - 1;
+        if (__builtin_amdgcn_readfirstlane(jl) == n_kb - 1) C -= 1;
+    }
 
     // Kept block indices through the scalar cache (wave-uniform addresses; the list
     // is read-only here).
@@ -368,12 +375,14 @@ __global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 4 : 2) attn_kernel(const A
     };
 
     int nv0 = 0, nv1 = 0;  // real keys of chunks ch and ch+1
+    int jnext = -1;        // block of chunk ch+1, read one chunk ahead
     // Chunk ch from slots (ks, vs); first the DMA of chunk ch+1 into (kd, vd), the
     // slots of chunk ch-1 (free since the barrier that ended it).
     auto iter = [&](auto z, int ch, const unsigned char *ks, const unsigned char *vs, unsigned char *kd,
                     unsigned char *vd) __attribute__((always_inline)) {
         if (ch + 1 < C) {
-            const int j1 = block_of(ch + 1);
+            const int j1 = jnext;
+            jnext = ch + 2 < C ? block_of(ch + 2) : -1;
             nv1 = __builtin_amdgcn_readfirstlane(chunk_keys(j1, ch + 1));
             const int row1 = chunk_row0(j1, ch + 1);
             dma_chunk(krs, row1, kd);
@@ -406,6 +415,7 @@ __global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 4 : 2) attn_kernel(const A
             const int row0 = chunk_row0(j0, 0);
             dma_chunk(krs, row0, k_s0);
             dma_chunk(vrs, row0, v_s0);
+            jnext = C > 1 ? block_of(1) : -1;
         }
         wait_vm_all();
         __syncthreads();
