@@ -11,8 +11,9 @@
 //
 // Keys are consumed in 64-key chunks (one 64-key block of the kept list, or half
 // of a 128-key block). A chunk is two 32-key sub-tiles; for each, a wave issues
-// its 4 score MFMAs, forms the probabilities and issues its 4 PV MFMAs, in that
-// order. Latency is hidden by occupancy rather than by pipelining inside a wave:
+// its 4 score MFMAs, forms the probabilities and issues its 4 PV MFMAs (the score
+// MFMAs of the second sub-tile go ahead of the PV MFMAs of the first). Latency is
+// hidden by occupancy rather than by a software pipeline across chunks:
 // K and V chunks sit in two-slot rings of 8 KB per tensor and slot (32 KB per
 // workgroup), and the kernel fits 128 registers, so four 128-query workgroups
 // share a CU (four waves per SIMD), and the matrix and vector pipes of a SIMD
@@ -388,21 +389,26 @@ __global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 4 : 2) attn_kernel(const A
             dma_chunk(krs, row1, kd);
             dma_chunk(vrs, row1, vd);
         }
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            f32x16 s;
-            bf16x8 pb[2];
-            qk(ks, t, s);
-            if (nv0 < 64) {
-                // A real branch: only partial chunks pay for the mask (the empty asm
-                // keeps the compiler from if-converting it into every sub-tile).
-                asm volatile("" ::: "memory");
-                mask(s, nv0, t);
-            }
-            const float lh = probs(z, s, pb);
-            settle(z, s, pb, lh);
-            pv(vs, t, pb);
+        // Sub-tile 0, then the score MFMAs of sub-tile 1 ahead of the PV MFMAs of
+        // sub-tile 0, so that the softmax of sub-tile 1 can start while those run.
+        // Partial chunks pay for the mask on a real branch (the empty asm keeps the
+        // compiler from if-converting it into every sub-tile).
+        f32x16 s0, s1;
+        bf16x8 p0[2], p1[2];
+        qk(ks, 0, s0);
+        if (nv0 < 64) {
+            asm volatile("" ::: "memory");
+            mask(s0, nv0, 0);
         }
+        settle(z, s0, p0, probs(z, s0, p0));
+        qk(ks, 1, s1);
+        pv(vs, 0, p0);
+        if (nv0 < 64) {
+            asm volatile("" ::: "memory");
+            mask(s1, nv0, 1);
+        }
+        settle(z, s1, p1, probs(z, s1, p1));
+        pv(vs, 1, p1);
         wait_vm_all();    // this wave's loads of chunk ch+1 have landed
         __syncthreads();  // ... and every wave's; chunk ch's slots are no longer read
         nv0 = nv1;
