@@ -229,11 +229,13 @@ __global__ void __launch_bounds__(BQ * 2, BQ == 128 ? 4 : 2) attn_kernel(const A
         return valid(j) ? max(0, min(64, N - j * BK - 64 * (ch & (CPE - 1)))) : 0;
     };
 
-    // This head's K and V as buffer resources (byte offsets below N * 128 < 2^31).
+    // This head's K and V as buffer resources: N * 128 bytes (at most 2^31 for
+    // N <= 2^24, as a 32-bit unsigned record count; row offsets stay below 2^31).
+    const int head_bytes = (int)((unsigned int)N * 128u);
     const __amdgpu_buffer_rsrc_t krs =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k + head * kD), 0, N * 128, 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k + head * kD), 0, head_bytes, 0x00020000);
     const __amdgpu_buffer_rsrc_t vrs =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v + head * kD), 0, N * 128, 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v + head * kD), 0, head_bytes, 0x00020000);
     // DMA lane constants: load u of a thread fills row r0 + 8 NW u of the slot, at
     // physical chunk lane & 7, from source chunk (lane & 7) ^ swz(row) (the same for
     // every u: the swizzle depends on row bits 1-3 only).
